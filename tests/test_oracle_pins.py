@@ -1,0 +1,533 @@
+"""Pins of the CPU oracle to facts fixed by the paper and by mathematics.
+
+Each check is written once as a function of the oracle routine(s) it pins, so
+that the mutation tests at the end can plant a plausible mistake in a copy of
+the oracle and show that the same check fails.  Nothing here calls the GPU.
+"""
+import math
+import statistics
+
+import numpy as np
+import pytest
+
+import oracle as orc
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _harmonic(n):
+    return math.fsum(1.0 / i for i in range(1, n + 1))
+
+
+# --------------------------------------------------------------------------
+# S1: window scores
+# --------------------------------------------------------------------------
+
+def check_zero_query_closed_form(window_scores):
+    """Q = 0: every visible logit is 0, so row r at position p has A = 1/(p+1).
+    P[t]  = (H_T - H_{T-O}) / O for every candidate t (all base rows see t);
+    P'[t] = (H_T - H_{max(t, T-O')}) / O'  (causal edge of the extended window);
+    I[t]  = P[t] (every head is identical).  H_n is the n-th harmonic number."""
+    T, wn, O, hkv, g, d = 53, 10, 4, 3, 2, 8
+    k = _rng(1).standard_normal((hkv, T, d))
+    q = np.zeros((hkv * g, wn, d))
+    p, pe, imp = window_scores(q, k, O)
+    Tc = T - O
+    want_p = (_harmonic(T) - _harmonic(T - O)) / O
+    want_pe = np.array([(_harmonic(T) - _harmonic(max(t, T - wn))) / wn for t in range(Tc)])
+    assert p.shape == (hkv, Tc) and pe.shape == (hkv, Tc) and imp.shape == (Tc,)
+    np.testing.assert_allclose(p, want_p, rtol=1e-13, atol=0)
+    np.testing.assert_allclose(pe, np.broadcast_to(want_pe, pe.shape), rtol=1e-13, atol=0)
+    np.testing.assert_allclose(imp, want_p, rtol=1e-13, atol=0)
+
+
+def _brute_scores(q, k, O):
+    """Pure-Python loops: causal softmax per query head, mean over the G heads of a
+    KV head, window sums, max over KV heads.  Shares nothing with the oracle."""
+    hq, wn, d = len(q), len(q[0]), len(q[0][0])
+    hkv, T = len(k), len(k[0])
+    g = hq // hkv
+    abar = [[[0.0] * T for _ in range(wn)] for _ in range(hkv)]
+    for j in range(hq):
+        h = j // g
+        for r in range(wn):
+            p = T - wn + r
+            logits = [math.fsum(q[j][r][i] * k[h][t][i] for i in range(d)) / math.sqrt(d)
+                      for t in range(p + 1)]
+            mx = max(logits)
+            ex = [math.exp(x - mx) for x in logits]
+            z = math.fsum(ex)
+            for t in range(p + 1):
+                abar[h][r][t] += ex[t] / z / g
+    Tc = T - O
+    P = [[math.fsum(abar[h][r][t] for r in range(wn - O, wn)) / O for t in range(Tc)]
+         for h in range(hkv)]
+    PE = [[math.fsum(abar[h][r][t] for r in range(wn)) / wn for t in range(Tc)] for h in range(hkv)]
+    I = [math.fsum(max(abar[h][r][t] for h in range(hkv)) for r in range(wn - O, wn)) / O
+         for t in range(Tc)]
+    return np.array(P), np.array(PE), np.array(I)
+
+
+def check_brute_force(window_scores):
+    for seed, (T, wn, O, hkv, g, d) in enumerate([(17, 5, 2, 2, 2, 4), (23, 7, 3, 3, 1, 6),
+                                                  (12, 12, 4, 2, 3, 4), (9, 4, 4, 1, 4, 2)]):
+        r = _rng(100 + seed)
+        q = r.standard_normal((hkv * g, wn, d)) * 2.0
+        k = r.standard_normal((hkv, T, d)) * 2.0
+        p, pe, imp = window_scores(q, k, O)
+        bp, bpe, bimp = _brute_scores(q.tolist(), k.tolist(), O)
+        np.testing.assert_allclose(p, bp, rtol=1e-11, atol=1e-300)
+        np.testing.assert_allclose(pe, bpe, rtol=1e-11, atol=1e-300)
+        np.testing.assert_allclose(imp, bimp, rtol=1e-11, atol=1e-300)
+
+
+def check_mass(window_scores):
+    """Each query row's attention sums to 1, so over all T tokens P and P' sum to 1."""
+    r = _rng(7)
+    q = r.standard_normal((8, 12, 16)) * 3
+    k = r.standard_normal((4, 300, 16))
+    p, pe, imp = window_scores(q, k, 5, full=True)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, rtol=1e-13)
+    np.testing.assert_allclose(pe.sum(axis=1), 1.0, rtol=1e-13)
+    assert np.all(imp >= p.max(axis=0) * (1 - 1e-14))   # max over heads >= each head
+
+
+def check_identical_heads(window_scores):
+    """All KV heads (and their query groups) identical: I equals every head's P."""
+    r = _rng(9)
+    k1 = r.standard_normal((1, 64, 8))
+    q1 = r.standard_normal((2, 6, 8))
+    k = np.repeat(k1, 3, axis=0)
+    q = np.concatenate([q1] * 3, axis=0)
+    p, pe, imp = window_scores(q, k, 3)
+    for h in range(3):
+        np.testing.assert_allclose(p[h], imp, rtol=1e-14)
+    p1, _, imp1 = window_scores(q1, k1, 3)
+    np.testing.assert_allclose(imp1, p1[0], rtol=1e-14)
+
+
+def check_single_row_softmax(window_scores):
+    """O = O' = 1 and G = 1: P is the plain softmax of the last row over t < T-1."""
+    r = _rng(11)
+    q = r.standard_normal((1, 1, 8))
+    k = r.standard_normal((1, 40, 8))
+    p, pe, imp = window_scores(q, k, 1)
+    s = (k[0] @ q[0, 0]) / math.sqrt(8)
+    e = np.exp(s - s.max())
+    sm = e / e.sum()
+    np.testing.assert_allclose(p[0], sm[:39], rtol=1e-13)
+    np.testing.assert_allclose(pe[0], sm[:39], rtol=1e-13)
+
+
+def test_zero_query_closed_form():
+    check_zero_query_closed_form(orc.window_scores)
+
+
+def test_window_scores_brute_force():
+    check_brute_force(orc.window_scores)
+
+
+def test_mass_identity():
+    check_mass(orc.window_scores)
+
+
+def test_identical_heads():
+    check_identical_heads(orc.window_scores)
+
+
+def test_single_row_softmax():
+    check_single_row_softmax(orc.window_scores)
+
+
+def test_head_permutation_equivariance():
+    r = _rng(12)
+    hkv, g = 4, 2
+    q = r.standard_normal((hkv * g, 6, 8))
+    k = r.standard_normal((hkv, 50, 8))
+    perm = np.array([2, 0, 3, 1])
+    qperm = q.reshape(hkv, g, 6, 8)[perm].reshape(hkv * g, 6, 8)
+    p, pe, imp = orc.window_scores(q, k, 3)
+    p2, pe2, imp2 = orc.window_scores(qperm, k[perm], 3)
+    np.testing.assert_allclose(p2, p[perm], rtol=1e-13)
+    np.testing.assert_allclose(pe2, pe[perm], rtol=1e-13)
+    np.testing.assert_allclose(imp2, imp, rtol=1e-13)
+
+
+def test_to_f32_round_to_nearest_even():
+    x = np.array([1.0 + 2.0 ** -24, 1.0 + 3 * 2.0 ** -24, 1.0 + 2.0 ** -25])
+    y = orc.to_f32(x)
+    assert y.dtype == np.float32
+    assert y[0] == np.float32(1.0)                      # tie -> even
+    assert y[1] == np.float32(1.0 + 2.0 ** -22)         # tie -> even (up)
+    assert y[2] == np.float32(1.0)
+
+
+# --------------------------------------------------------------------------
+# S2: max pooling
+# --------------------------------------------------------------------------
+
+def check_maxpool(maxpool1d):
+    r = _rng(13)
+    for n, kern in [(1, 7), (5, 7), (20, 5), (33, 7), (10, 1), (9, 3)]:
+        x = r.integers(0, 6, size=(2, n)).astype(np.float32)   # many exact ties
+        got = maxpool1d(x, kern)
+        rad = kern // 2
+        want = np.array([[max(x[h, max(0, t - rad):min(n, t + rad + 1)]) for t in range(n)]
+                         for h in range(2)], dtype=np.float32)
+        np.testing.assert_array_equal(got, want)
+
+
+def test_maxpool_naive():
+    check_maxpool(orc.maxpool1d)
+
+
+def test_maxpool_identity_kernel_one():
+    x = _rng(14).standard_normal((3, 17)).astype(np.float32)
+    np.testing.assert_array_equal(orc.maxpool1d(x, 1), x)
+
+
+# --------------------------------------------------------------------------
+# S3: head focus and the adjusted heads
+# --------------------------------------------------------------------------
+
+def check_sigma(head_sigma):
+    r = _rng(15)
+    x = r.random((5, 31)).astype(np.float32)
+    got = head_sigma(x)
+    for h in range(5):
+        want = statistics.pstdev([float(v) for v in x[h]])   # exact rational arithmetic
+        assert abs(got[h] - want) <= 1e-15 * max(want, 1e-30) + 1e-17
+
+
+def check_lowest_sigma(adjusted_heads):
+    """H_top holds the delta heads with the LOWEST sigma (Sec. 4.1); ties -> lower head."""
+    s = np.array([3.0, 1.0, 2.0, 1.0, 0.5])
+    assert list(adjusted_heads(s, 2)) == [1, 4]
+    assert list(adjusted_heads(s, 3)) == [1, 3, 4]
+    assert list(adjusted_heads(s, 0)) == []
+    assert list(adjusted_heads(s, 9)) == [0, 1, 2, 3, 4]
+
+
+def test_sigma_population_std():
+    check_sigma(orc.head_sigma)
+
+
+def test_adjusted_heads_lowest_sigma():
+    check_lowest_sigma(orc.adjusted_heads)
+
+
+# --------------------------------------------------------------------------
+# S4/S6: ranking
+# --------------------------------------------------------------------------
+
+def check_rank_brute(rank_first):
+    """Brute force: t is among the first k iff fewer than k tokens precede it in the
+    order (score desc, index asc)."""
+    r = _rng(16)
+    for n in [1, 2, 7, 30, 64]:
+        s = r.integers(0, 5, size=n).astype(np.float32)
+        for k in [0, 1, n // 2, n]:
+            got = set(int(i) for i in rank_first(s, k))
+            want = set()
+            for t in range(n):
+                ahead = sum(1 for u in range(n) if s[u] > s[t] or (s[u] == s[t] and u < t))
+                if ahead < k:
+                    want.add(t)
+            assert got == want, (n, k)
+            assert len(rank_first(s, k)) == k
+
+
+def test_rank_first_brute_force():
+    check_rank_brute(orc.rank_first)
+
+
+def test_preserve_count():
+    assert orc.preserve_count(128, 32, 0.25) == 32
+    assert orc.preserve_count(1024, 32, 0.25) == 256
+    assert orc.preserve_count(512, 64, 0.25) == 128
+    assert orc.preserve_count(2048, 32, 0.25) == 512
+    assert orc.preserve_count(128, 32, 1.0) == 96       # capped at B - O
+    assert orc.preserve_count(128, 32, 0.0) == 0
+
+
+# --------------------------------------------------------------------------
+# S5: cross-layer bonus
+# --------------------------------------------------------------------------
+
+def check_bonus_hand(adjusted_priority):
+    """Hand-computed, exactly representable cases of P' = P + lambda*I*(1 - n/(l+1))."""
+    p = np.array([[0.25, 0.5, 0.125, 0.0]], dtype=np.float32)
+    imp = np.array([0.5, 0.25, 1.0, 0.75], dtype=np.float32)
+    n = np.array([1, 0, 3, 2])
+    keep = np.zeros((1, 4), dtype=bool)
+    # layer 3 -> denominator 4: coverage = 1/4, 0, 3/4, 2/4
+    got = adjusted_priority(p, imp, n, 3, 2.0, keep)
+    want = np.array([[0.25 + 2 * 0.5 * 0.75, 0.5 + 2 * 0.25, 0.125 + 2 * 1.0 * 0.25,
+                      0.0 + 2 * 0.75 * 0.5]], dtype=np.float32)
+    np.testing.assert_array_equal(got, want)
+    keep[0, 2] = True
+    got = adjusted_priority(p, imp, n, 3, 2.0, keep)
+    assert got[0, 2] == np.float32(1.0)
+    # layer 0: nothing covered yet -> focus = I
+    got0 = adjusted_priority(p, imp, np.zeros(4, int), 0, 1.0, np.zeros((1, 4), bool))
+    np.testing.assert_array_equal(got0, (p + imp[None, :]).astype(np.float32))
+    # lambda = 0 leaves P untouched
+    got1 = adjusted_priority(p, imp, n, 3, 0.0, np.zeros((1, 4), bool))
+    np.testing.assert_array_equal(got1, p)
+
+
+def test_bonus_hand():
+    check_bonus_hand(orc.adjusted_priority)
+
+
+def test_bonus_fp32_single_rounding():
+    """Each operation is one fp32 operation: compare with explicit fp32 steps
+    computed through Python floats rounded after every operation."""
+    r = _rng(17)
+    p = r.random((2, 50)).astype(np.float32) * 1e-3
+    imp = r.random(50).astype(np.float32) * 1e-2
+    n = r.integers(0, 7, size=50)
+    got = orc.adjusted_priority(p, imp, n, 6, 1.0, np.zeros((2, 50), bool))
+    f = lambda v: float(np.float32(v))   # noqa: E731
+    for h in range(2):
+        for t in range(50):
+            cov = f(f(n[t]) / f(7))
+            want = f(f(p[h, t]) + f(f(1.0) * f(f(imp[t]) * f(1.0 - cov))))
+            assert got[h, t] == np.float32(want)
+
+
+# --------------------------------------------------------------------------
+# whole layer on fp32 scores
+# --------------------------------------------------------------------------
+
+def _scores(seed, H, Tc, heavy=True):
+    r = _rng(seed)
+    p = (r.random((H, Tc)) ** 4 * 1e-3).astype(np.float32)
+    pe = (p * (0.5 + r.random((H, Tc)))).astype(np.float32)
+    imp = (p.max(axis=0) * (1 + r.random(Tc))).astype(np.float32)
+    return p, pe, imp
+
+
+def _sel(p, pe, imp, n_t, layer, **kw):
+    return orc.select_layer(p, pe, imp, n_t, layer, **kw)
+
+
+def test_layer_invariants():
+    H, T, O, B = 4, 300, 8, 40
+    p, pe, imp = _scores(18, H, T - O)
+    n_t = _rng(19).integers(0, 3, size=T)
+    res = _sel(p, pe, imp, n_t, 2, T=T, window=O, window_ext=16, budget=B, pool_kernel=5,
+               delta=2, lam=1.0, beta=0.25)
+    assert res.idx.shape == (H, B)
+    for h in range(H):
+        row = res.idx[h]
+        assert len(set(row.tolist())) == B                    # exactly B distinct tokens
+        assert list(row[B - O:]) == list(range(T - O, T))     # the window is kept
+        pre = row[:B - O]
+        assert np.all(np.diff(pre) > 0) and pre[-1] < T - O   # ascending prefix picks
+        assert res.keep[h].sum() == orc.preserve_count(B, O, 0.25)
+        assert set(np.nonzero(res.keep[h])[0].tolist()) <= set(pre.tolist())
+    assert len(res.htop) == 2
+    assert res.bits.sum() == len(set(res.idx.ravel().tolist()))
+
+
+def test_reduces_to_snapkv_when_coverage_off():
+    """delta = 0 and lambda = 0: plain top-(B-O) of the pooled window score, plus the window."""
+    H, T, O, B = 3, 200, 6, 30
+    p, pe, imp = _scores(20, H, T - O)
+    n_t = _rng(21).integers(0, 4, size=T)
+    res = _sel(p, pe, imp, n_t, 3, T=T, window=O, window_ext=12, budget=B, pool_kernel=7,
+               delta=0, lam=0.0, beta=0.25)
+    pooled = orc.maxpool1d(p, 7)
+    for h in range(H):
+        want = np.sort(orc.rank_first(pooled[h], B - O))
+        np.testing.assert_array_equal(res.idx[h, :B - O], want)
+
+
+def test_full_preserve_ignores_bonus():
+    """beta*B >= B-O: every prefix pick is preserved, so the bonus cannot change the set."""
+    H, T, O, B = 3, 150, 4, 20
+    p, pe, imp = _scores(22, H, T - O)
+    n_t = np.zeros(T, int)
+    a = _sel(p, pe, imp, n_t, 0, T=T, window=O, window_ext=8, budget=B, pool_kernel=3,
+             delta=1, lam=5.0, beta=1.0)
+    b = _sel(p, pe, imp, n_t, 0, T=T, window=O, window_ext=8, budget=B, pool_kernel=3,
+             delta=1, lam=0.0, beta=1.0)
+    np.testing.assert_array_equal(a.idx, b.idx)
+
+
+def check_preserve_uses_replaced_scores(select_layer):
+    """Algorithm 1 replaces P by the extended-window score for H_top BEFORE picking the
+    preserved tokens, so a head in H_top preserves its top tokens of P_ext."""
+    T, O, B = 40, 2, 6          # 4 prefix picks, preserve 1 (beta = 0.25 -> floor(1.5) = 1)
+    Tc = T - O
+    p = np.full((2, Tc), 1e-3, np.float32)
+    p[1, ::5] = 0.2             # head 1 is focused; head 0 (flat) has the lowest sigma
+    p[0, 10] = 2e-3             # head 0's best token under P
+    pe = p.copy()
+    pe[0, 30] = 0.05            # head 0's best token under P_ext
+    imp = np.zeros(Tc, np.float32)
+    imp[12] = 0.9               # a big bonus elsewhere
+    res = select_layer(p, pe, imp, np.zeros(T, int), 0, T=T, window=O, window_ext=4, budget=B,
+                       pool_kernel=1, delta=1, lam=1.0, beta=0.25)
+    assert list(res.htop) == [0]
+    assert res.keep[0, 30] and not res.keep[0, 10]
+    assert 30 in res.idx[0]
+
+
+def test_preserve_uses_replaced_scores():
+    check_preserve_uses_replaced_scores(orc.select_layer)
+
+
+def test_preserve_beats_bonus():
+    """A preserved token stays even when the coverage bonus lifts others above it."""
+    T, O, B = 30, 2, 4          # 2 prefix picks, beta = 0.25 -> preserve 1
+    Tc = T - O
+    p = np.full((1, Tc), 1e-4, np.float32)
+    p[0, 5] = 0.3
+    imp = np.zeros(Tc, np.float32)
+    imp[[9, 11]] = 0.8
+    res = orc.select_layer(p, p, imp, np.zeros(T, int), 0, T=T, window=O, window_ext=O, budget=B,
+                           pool_kernel=1, delta=0, lam=1.0, beta=0.25)
+    assert list(res.idx[0, :2]) == [5, 9]       # without preservation: [9, 11]
+
+
+def test_keep_everything_when_budget_covers_prefix():
+    H, T, O, B = 2, 20, 4, 32
+    p, pe, imp = _scores(23, H, T - O)
+    res = _sel(p, pe, imp, np.zeros(T, int), 0, T=T, window=O, window_ext=8, budget=B,
+               pool_kernel=3, delta=1, lam=1.0, beta=0.25)
+    assert list(res.idx[0, :T]) == list(range(T))
+    assert np.all(res.idx[:, T:] == -1)
+
+
+def test_coverage_is_union_size():
+    r = _rng(24)
+    T = 100
+    layers = []
+    for _ in range(4):
+        idx = np.stack([np.sort(r.choice(T, 10, replace=False)) for _ in range(3)]).astype(np.int32)
+        layers.append(orc.layer_bits(idx, T))
+    want = len(set().union(*[set(np.nonzero(b)[0].tolist()) for b in layers]))
+    assert orc.coverage_count(layers) == want
+    n_t = orc.counts_from_bits(layers[:3])
+    assert n_t.max() <= 3
+
+
+def test_gather_rows():
+    x = _rng(25).standard_normal((2, 10, 4))
+    idx = np.array([[3, 1, 9, -1], [0, 0, 5, 2]], dtype=np.int32)
+    g = orc.gather_rows(x, idx)
+    np.testing.assert_array_equal(g[0, 0], x[0, 3])
+    np.testing.assert_array_equal(g[1, 2], x[1, 5])
+    assert np.all(g[0, 3] == 0)
+
+
+# --------------------------------------------------------------------------
+# mutation tests: a planted mistake in a copy of the oracle must fail a pin
+# --------------------------------------------------------------------------
+
+def _mut_no_causal(q_win, k, window, full=False):
+    hq, wn, d = q_win.shape
+    hkv, T, _ = k.shape
+    g = hq // hkv
+    abar = np.zeros((hkv, wn, T))
+    for j in range(hq):
+        s = (q_win[j] @ k[j // g].T) / math.sqrt(d)          # mistake: no causal mask
+        e = np.exp(s - s.max(axis=1, keepdims=True))
+        abar[j // g] += e / e.sum(axis=1, keepdims=True) / g
+    O = window
+    p = abar[:, wn - O:].sum(1) / O
+    pe = abar.sum(1) / wn
+    imp = abar[:, wn - O:].max(0).sum(0) / O
+    tc = T if full else T - O
+    return p[:, :tc], pe[:, :tc], imp[:tc]
+
+
+def _mut_wrong_window(q_win, k, window, full=False):
+    p, pe, imp = orc.window_scores(q_win, k, window, full)
+    return pe, pe, imp                                       # mistake: P over O' rows
+
+
+def _mut_query_head_max(q_win, k, window, full=False):
+    hq, wn, d = q_win.shape
+    hkv, T, _ = k.shape
+    g = hq // hkv
+    pos = T - wn + np.arange(wn)
+    vis = np.arange(T)[None, :] <= pos[:, None]
+    a = np.zeros((hq, wn, T))
+    for j in range(hq):
+        s = np.where(vis, (q_win[j] @ k[j // g].T) / math.sqrt(d), -np.inf)
+        e = np.exp(s - s.max(1, keepdims=True))
+        a[j] = e / e.sum(1, keepdims=True)
+    abar = a.reshape(hkv, g, wn, T).mean(1)
+    O = window
+    p = abar[:, wn - O:].sum(1) / O
+    pe = abar.sum(1) / wn
+    imp = a[:, wn - O:].max(0).sum(0) / O                   # mistake: max over query heads
+    tc = T if full else T - O
+    return p[:, :tc], pe[:, :tc], imp[:tc]
+
+
+def _mut_highest_sigma(sigma, delta):
+    order = sorted(range(len(sigma)), key=lambda h: (-float(sigma[h]), h))   # mistake
+    return np.array(sorted(order[:delta]), dtype=np.int64)
+
+
+def _mut_layer_denominator(p_sel, imp, n_t, layer, lam, keep):
+    f32 = np.float32
+    cov = n_t.astype(f32) / f32(max(layer, 1))               # mistake: l instead of l+1
+    out = p_sel.astype(f32) + f32(lam) * (imp.astype(f32) * (f32(1) - cov))[None, :]
+    out[keep] = f32(1)
+    return out
+
+
+def _mut_sample_std(p):
+    x = np.asarray(p, dtype=np.float64)
+    return x.std(axis=1, ddof=1)                              # mistake: sample std
+
+
+def _mut_rank_index_desc(scores, k):
+    n = scores.shape[0]
+    return np.lexsort((-np.arange(n), -np.asarray(scores, np.float64)))[:k]   # mistake: ties
+
+
+def _mut_maxpool_shift(x, kernel):
+    out = orc.maxpool1d(x, kernel)
+    return np.concatenate([out[..., 1:], out[..., -1:]], axis=-1)            # mistake: off by one
+
+
+def _mut_preserve_raw(p_raw, p_ext_raw, imp, n_t, layer, **kw):
+    """Mistake: preserve set taken from P before the H_top replacement."""
+    res = orc.select_layer(p_raw, p_ext_raw, imp, n_t, layer, **kw)
+    H, Tc = p_raw.shape
+    pooled = orc.maxpool1d(p_raw.astype(np.float32), kw["pool_kernel"])
+    kp = orc.preserve_count(kw["budget"], kw["window"], kw["beta"])
+    keep = np.zeros((H, Tc), bool)
+    for h in range(H):
+        keep[h, orc.rank_first(pooled[h], kp)] = True
+    res.keep = keep
+    padj = orc.adjusted_priority(res.p_sel, imp, np.asarray(n_t)[:Tc], layer, kw["lam"], keep)
+    m = kw["budget"] - kw["window"]
+    for h in range(H):
+        res.idx[h, :m] = np.sort(orc.rank_first(padj[h], m))
+    return res
+
+
+@pytest.mark.parametrize("check,mutant", [
+    (check_zero_query_closed_form, _mut_no_causal),
+    (check_zero_query_closed_form, _mut_wrong_window),
+    (check_brute_force, _mut_no_causal),
+    (check_brute_force, _mut_query_head_max),
+    (check_lowest_sigma, _mut_highest_sigma),
+    (check_bonus_hand, _mut_layer_denominator),
+    (check_sigma, _mut_sample_std),
+    (check_rank_brute, _mut_rank_index_desc),
+    (check_maxpool, _mut_maxpool_shift),
+    (check_preserve_uses_replaced_scores, _mut_preserve_raw),
+])
+def test_pins_catch_planted_mistakes(check, mutant):
+    with pytest.raises(AssertionError):
+        check(mutant)
