@@ -1,0 +1,191 @@
+"""Throughput of the full K-VEC prefill eviction step on one MI355X.
+
+One step = window scores for every layer, then the coverage-aware selection
+of every layer in order (each layer reads the coverage bitmap of the earlier
+ones) and the gather of the kept K/V into the compacted cache: every stage of
+the hot path, on synthetic Llama-3.1-8B-shaped inputs resident in HBM.
+
+Prints one JSON line: prefix tokens/s (batch * T per step / step time), the
+roofline of the dominant kernel (live HIP-event timing), and the CPU oracle
+timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+
+
+def _hip():
+    lib = ctypes.CDLL("libamdhip64.so")
+    lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    return lib
+
+
+def _events(hip, n):
+    out = []
+    for _ in range(n):
+        e = ctypes.c_void_p()
+        assert hip.hipEventCreate(ctypes.byref(e)) == 0
+        out.append(e.value)
+    return out
+
+
+def _elapsed(hip, a, b) -> float:
+    ms = ctypes.c_float()
+    assert hip.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+    return ms.value
+
+
+def cpu_baseline(w, sample_layers: int):
+    """The oracle as it stands, on `sample_layers` layers of sequence 0."""
+    import numpy as np
+    import threadpoolctl
+
+    import oracle as orc
+    import synth
+    t_work = 0.0
+    prev = []
+    for l in range(sample_layers):
+        q = synth.to_f64(synth.queries(w, l, 0), w.dtype)
+        k = synth.to_f64(synth.keys(w, l, 0), w.dtype)
+        v = synth.values(w, l, 0)
+        t0 = time.perf_counter()
+        p, pe, imp = orc.score_layer(q, k, w.window)
+        n_t = orc.counts_from_bits(prev) if prev else np.zeros(w.seq_len, np.int64)
+        res = orc.evict_layer_from_scores(p, pe, imp, n_t, l, w)
+        orc.gather_rows(k, res.idx)
+        orc.gather_rows(v, res.idx)
+        t_work += time.perf_counter() - t0
+        prev.append(res.bits)
+    per_layer = t_work / sample_layers
+    step_s = per_layer * w.n_layers * w.batch
+    threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    return {"value": w.batch * w.seq_len / step_s, "unit": "prefix tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{sample_layers} of {w.n_layers} layers of sequence 0 "
+                      f"({t_work:.1f} s); extrapolated to {w.n_layers} layers x batch {w.batch}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=2, help="index of the synthetic workload")
+    ap.add_argument("--cpu-sample-layers", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU; multi-GPU runs are not part of this build "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2606_29563_amd import kvec
+
+    w = synth.workload(args.workload)
+    kvec.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    L, b, H, HQ, T, d, B = (w.n_layers, w.batch, w.n_kv_heads, w.n_q_heads, w.seq_len,
+                            w.head_dim, w.budget)
+    print(f"[bench] {w.name}: generating {L} layers of inputs", file=sys.stderr, flush=True)
+    q = torch.empty((L, b, HQ, w.rows, d), dtype=dt, device=dev)
+    k = torch.empty((L, b, H, T, d), dtype=dt, device=dev)
+    v = torch.empty_like(k)
+    for l in range(L):
+        for s in range(b):
+            for dst, arr in ((q, synth.queries(w, l, s)), (k, synth.keys(w, l, s)),
+                             (v, synth.values(w, l, s))):
+                t = torch.from_numpy(arr)
+                if w.dtype == "bf16":
+                    t = t.view(torch.bfloat16)
+                dst[l, s].copy_(t)
+    cfg = kvec.Config.from_workload(w)
+    ws = torch.empty(kvec.kvec_workspace_size(cfg), dtype=torch.uint8, device=dev)
+    bits = torch.empty((b, L, (T + 63) // 64), dtype=torch.int64, device=dev)
+    idx = torch.empty((L, b, H, B), dtype=torch.int32, device=dev)
+    ko = torch.empty((L, b, H, B, d), dtype=dt, device=dev)
+    vo = torch.empty_like(ko)
+    torch.cuda.synchronize()
+    print("[bench] inputs resident; warming up", file=sys.stderr, flush=True)
+
+    hip = _hip()
+    evs = [_events(hip, 4 * L) for _ in range(args.steps)]
+    for _ in range(args.warmup):
+        kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws, events=evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    print(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms", file=sys.stderr, flush=True)
+
+    # Per-kernel durations of the two score passes (HIP events on the library's stream).
+    p1 = p2 = 0.0
+    for s in range(args.steps):
+        e = evs[s]
+        for l in range(L):
+            p1 += _elapsed(hip, e[4 * l], e[4 * l + 1])
+            p2 += _elapsed(hip, e[4 * l + 2], e[4 * l + 3])
+    n = args.steps * L
+    p1, p2 = p1 / n, p2 / n
+    es = 2 if w.dtype == "bf16" else 4
+    Tc = T - w.window
+    k_bytes_p1 = b * H * T * d * es + b * HQ * w.rows * d * es
+    k_bytes_p2 = b * H * Tc * d * es + b * HQ * w.rows * d * es
+    if p2 >= p1:
+        kern, dur, byts = "score pass 2 (probabilities, window sums, head max)", p2, k_bytes_p2
+    else:
+        kern, dur, byts = "score pass 1 (row normalisers)", p1, k_bytes_p1
+    achieved = byts / (dur * 1e-3) / 1e9
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kern,
+            "avg_launch_us": round(dur * 1e3, 2),
+            "pass1_us": round(p1 * 1e3, 2), "pass2_us": round(p2 * 1e3, 2)}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        # about 10 s of oracle work (~5e-5 s per token and layer on 8 cores)
+        sample = args.cpu_sample_layers or max(1, min(L, round(10.0 / (5e-5 * T))))
+        print(f"[bench] CPU oracle on {sample} layer(s)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, sample)
+
+    tokens = b * T
+    out = {
+        "metric": "prefix tokens/s through full eviction step (all layers); % HBM/MFMA roofline",
+        "value": round(tokens / (ms_step * 1e-3), 1), "unit": "prefix tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "batch": b, "kv_heads": H, "q_heads": HQ,
+                   "head_dim": d, "seq_len": T, "window": w.window, "window_ext": w.window_ext,
+                   "budget": B, "pool": w.pool_kernel, "delta": w.n_adjust_heads,
+                   "lambda": w.lam, "beta": w.beta},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

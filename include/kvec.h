@@ -1,0 +1,178 @@
+/*
+ * libkvec — prefill-time KV-cache eviction with coverage (K-VEC) on MI355X.
+ *
+ * C ABI.  Plain pointers and sizes; device pointers are HIP device memory
+ * (hipMalloc or a framework allocator), host pointers are ordinary memory.
+ *
+ * What the library computes (paper: "Coverage-Driven KV Cache Eviction for
+ * Efficient and Improved Inference of LLM"):
+ *
+ *   kvec_score        the windowed eviction score P (Sec. 4.1, Eq. eviction),
+ *                     the same score over the extended window O' (Sec. 4.1,
+ *                     cross-head coverage) and the global importance I
+ *                     (Sec. 4.2), for every KV head of one layer.
+ *   kvec_select_cover the rest of Algorithm 1 on those scores: max-pooling,
+ *                     head focus sigma, the delta lowest-sigma heads H_top
+ *                     switched to the extended-window score, the preserve set
+ *                     (top beta*B per head), the coverage bonus
+ *                     P' = P + lambda * I * (1 - n_t/(l+1)), then the top-B
+ *                     selection per head (Sec. 4.1) and the layer's entry in
+ *                     the token-coverage bitmap that defines n_t (Sec. 4.2).
+ *   kvec_compact      the cache store of the kept tokens (Sec. 4.1: the K/V of
+ *                     the selected B tokens is stored for decoding).
+ *   kvec_evict_layer  the three calls above for one layer.
+ *   kvec_evict_model  the whole prefill eviction step for all layers.
+ *   kvec_coverage     the coverage C = number of unique tokens kept across
+ *                     heads and layers (Sec. 3.2).
+ *
+ * Conventions common to every call
+ *   - Heads are KV heads.  Query head j belongs to KV head j / G with
+ *     G = n_q_heads / n_kv_heads; A of a KV head is the mean of its G query
+ *     heads' attention.  The observation window is the last O positions
+ *     [T-O, T); it is always kept, and each head keeps B-O more tokens chosen
+ *     from the candidates [0, T-O) ("Tc" below = T - O).
+ *   - Element strides are in elements, not bytes; the head dimension d is
+ *     contiguous.  Base pointers must be 16-byte aligned and every stride
+ *     times the element size a multiple of 16 bytes (KVEC_ERR_INVALID).
+ *   - Ownership: the caller owns every buffer.  The library never allocates
+ *     device memory and keeps no state between calls; scratch memory is the
+ *     caller's workspace `ws` of at least kvec_workspace_size() bytes.
+ *   - All device work is enqueued on `stream` and is asynchronous; no call
+ *     synchronises the host.  Calls on one workspace must be stream-ordered.
+ *   - Errors: argument validation happens before any launch; on a validation
+ *     error nothing is written.  A failed kernel launch returns
+ *     KVEC_ERR_DEVICE (outputs are then undefined).
+ *   - Ties: every ranking orders by (score descending, token index ascending);
+ *     sigma ties order by lower head index.
+ */
+#ifndef KVEC_H
+#define KVEC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kvec_status {
+  KVEC_OK = 0,
+  KVEC_ERR_INVALID = 1,      /* bad argument, shape, alignment or null pointer */
+  KVEC_ERR_UNSUPPORTED = 2,  /* valid but not implemented (head_dim, group size) */
+  KVEC_ERR_WORKSPACE = 3,    /* workspace smaller than kvec_workspace_size() */
+  KVEC_ERR_DEVICE = 4        /* a HIP launch or runtime call failed */
+} kvec_status;
+
+typedef enum kvec_dtype {
+  KVEC_BF16 = 0,  /* Q, K, V and the compacted cache are bfloat16 */
+  KVEC_F32 = 1    /* ... are IEEE float32 */
+} kvec_dtype;
+
+/* Shape and hyper-parameters of one eviction problem (Algorithm 1 inputs). */
+typedef struct kvec_config {
+  int32_t batch;          /* independent sequences, >= 1 */
+  int32_t n_layers;       /* L, >= 1 (rows of the coverage bitmap) */
+  int32_t n_kv_heads;     /* H, 1..16 */
+  int32_t n_q_heads;      /* multiple of H; G = n_q_heads / H in {1, 2, 4, 8} */
+  int32_t head_dim;       /* d in {64, 128} */
+  int32_t seq_len;        /* T, prefix length including the window, >= 1 */
+  int32_t window;         /* O, 1 <= O <= T */
+  int32_t window_ext;     /* O' >= O (clamped to T); O' == O turns cross-head off */
+  int32_t budget;         /* B per KV head including the window, B >= O */
+  int32_t pool_kernel;    /* odd, >= 1: max-pool width along t (1 = none) */
+  int32_t n_adjust_heads; /* delta, 0..H: heads switched to the O' score */
+  float lambda;           /* >= 0: cross-layer bonus weight (0 = off) */
+  float beta;             /* in [0, 1]: preserve K = min(floor(beta*B), B-O) per head */
+  int32_t dtype;          /* kvec_dtype of Q, K, V and the compacted cache */
+} kvec_config;
+
+/* Bytes of workspace the score/select/evict calls need for `cfg`.
+ * Host-only; never touches the device. */
+kvec_status kvec_workspace_size(const kvec_config* cfg, size_t* bytes);
+
+/* Window scores of one layer (Sec. 4.1 Eq. eviction and its O' variant;
+ * Sec. 4.2 global importance).
+ *   q_win      device, [batch][n_q_heads][O'][d] rows at positions T-O'..T-1
+ *              (post-RoPE), strides q_strides = {batch, head, row}.
+ *   k          device, [batch][H][T][d], strides k_strides = {batch, head, t}.
+ *   p_raw      device out, fp32 [batch][H][Tc]: P[h,t] = (1/O) sum over the
+ *              last O window rows of A (causal softmax, scale 1/sqrt(d)).
+ *   p_ext_raw  device out, fp32 [batch][H][Tc]: the same over all O' rows.
+ *   imp        device out, fp32 [batch][Tc]: I[t] = (1/O) sum over the last
+ *              O rows of the max over KV heads of A.
+ * Scores are not pooled.  Tc = T - O must be >= 1. */
+kvec_status kvec_score(const kvec_config* cfg,
+                       const void* q_win, const int64_t q_strides[3],
+                       const void* k, const int64_t k_strides[3],
+                       float* p_raw, float* p_ext_raw, float* imp,
+                       void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Selection of one layer from its scores (Algorithm 1, then top-B, Sec. 4.1-4.2).
+ *   layer       0-based index l; coverage uses n_t/(l+1).
+ *   p_raw, p_ext_raw, imp  device fp32, as written by kvec_score.
+ *   cover_bits  device uint64 [batch][n_layers][ceil(T/64)]: bit (l', t) set
+ *               when layer l' kept token t in at least one head.  Read for
+ *               layers < layer (n_t = number of those layers holding t),
+ *               written (atomic OR) for `layer`.  The caller zeroes the whole
+ *               bitmap before layer 0 and calls layers in increasing order.
+ *   idx         device out, int32 [batch][H][B]: the B-O prefix picks in
+ *               ascending order, then the window T-O..T-1.  If T <= B every
+ *               token is kept: 0..T-1, remaining slots -1.
+ *   htop_mask   device out, nullable, uint32 [batch]: bit h set when head h
+ *               used the extended-window score (H_top). */
+kvec_status kvec_select_cover(const kvec_config* cfg, int32_t layer,
+                              const float* p_raw, const float* p_ext_raw, const float* imp,
+                              uint64_t* cover_bits, int32_t* idx, uint32_t* htop_mask,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Cache store (Sec. 4.1): k_out[b][h][i] = k[b][h][idx[b][h][i]] and the same
+ * for v, byte-exact; rows with idx -1 are zero-filled.
+ *   k, v         device, [batch][H][T][d] with strides {batch, head, t}.
+ *   idx          device int32 [batch][H][B].
+ *   k_out, v_out device out, contiguous [batch][H][B][d]. */
+kvec_status kvec_compact(const kvec_config* cfg,
+                         const void* k, const int64_t k_strides[3],
+                         const void* v, const int64_t v_strides[3],
+                         const int32_t* idx, void* k_out, void* v_out, hipStream_t stream);
+
+/* One layer: kvec_score + kvec_select_cover + kvec_compact. */
+kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer,
+                             const void* q_win, const int64_t q_strides[3],
+                             const void* k, const int64_t k_strides[3],
+                             const void* v, const int64_t v_strides[3],
+                             uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The whole prefill eviction step: every layer in order 0..L-1.
+ *   q_win, k, v  device, strides {layer, batch, head, row/t}.
+ *   cover_bits   device uint64 [batch][L][ceil(T/64)]; zeroed by this call.
+ *   idx          device out int32 [L][batch][H][B].
+ *   k_out, v_out device out, contiguous [L][batch][H][B][d].
+ *   events       nullable; else 4*L caller-created HIP events recorded on
+ *                `stream` for profiling: for layer l, events[4l+0..1]
+ *                bracket the score pass that forms the row normalisers and
+ *                events[4l+2..3] the pass that forms the scores. */
+kvec_status kvec_evict_model(const kvec_config* cfg,
+                             const void* q_win, const int64_t q_strides[4],
+                             const void* k, const int64_t k_strides[4],
+                             const void* v, const int64_t v_strides[4],
+                             uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
+                             void* ws, size_t ws_bytes, hipStream_t stream,
+                             hipEvent_t* events);
+
+/* Coverage C (Sec. 3.2) per sequence over layers 0..upto_layer:
+ * count_per_seq[b] = popcount of the OR of those layers' bitmaps.
+ *   count_per_seq  device out, int64 [batch]. */
+kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits,
+                          int32_t upto_layer, int64_t* count_per_seq, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* kvec_status_string(kvec_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVEC_H */

@@ -1,0 +1,117 @@
+"""Host-only checks of the C ABI: the library loads, exports every declared
+entry point, and rejects bad arguments before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_29563_amd import kvec
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvec.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:kvec_status|const char\*)\s+(kvec_\w+)\s*\(", src, re.M)))
+
+
+def test_header_declares_expected_calls():
+    assert _declared() == sorted(kvec.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = kvec.load()
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_library_is_gfx950():
+    data = open(kvec.LIB_PATH, "rb").read()
+    assert b"gfx950" in data
+
+
+def _cfg(**kw):
+    base = dict(batch=1, n_layers=32, n_kv_heads=8, n_q_heads=32, head_dim=128, seq_len=32768,
+                window=32, window_ext=64, budget=1024, pool_kernel=7, n_adjust_heads=3, lam=1.0,
+                beta=0.25, dtype=kvec.KVEC_BF16)
+    base.update(kw)
+    return kvec.Config(**base)
+
+
+def _ws_status(cfg):
+    out = ctypes.c_size_t(0)
+    c = cfg.c()
+    return kvec.load().kvec_workspace_size(ctypes.byref(c), ctypes.byref(out)), out.value
+
+
+def test_workspace_size_positive_and_monotone():
+    s1, b1 = _ws_status(_cfg(seq_len=4096, budget=128))
+    s2, b2 = _ws_status(_cfg())
+    assert s1 == kvec.KVEC_OK and s2 == kvec.KVEC_OK
+    assert 0 < b1 < b2
+    assert kvec.kvec_workspace_size(_cfg()) == b2
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(batch=0), kvec.KVEC_ERR_INVALID),
+    (dict(n_layers=0), kvec.KVEC_ERR_INVALID),
+    (dict(n_layers=256), kvec.KVEC_ERR_INVALID),
+    (dict(n_q_heads=30), kvec.KVEC_ERR_INVALID),
+    (dict(window=0), kvec.KVEC_ERR_INVALID),
+    (dict(window=40000), kvec.KVEC_ERR_INVALID),
+    (dict(window_ext=16), kvec.KVEC_ERR_INVALID),
+    (dict(budget=16), kvec.KVEC_ERR_INVALID),
+    (dict(pool_kernel=6), kvec.KVEC_ERR_INVALID),
+    (dict(pool_kernel=0), kvec.KVEC_ERR_INVALID),
+    (dict(n_adjust_heads=-1), kvec.KVEC_ERR_INVALID),
+    (dict(n_adjust_heads=9), kvec.KVEC_ERR_INVALID),
+    (dict(lam=-1.0), kvec.KVEC_ERR_INVALID),
+    (dict(lam=float("nan")), kvec.KVEC_ERR_INVALID),
+    (dict(beta=1.5), kvec.KVEC_ERR_INVALID),
+    (dict(dtype=7), kvec.KVEC_ERR_INVALID),
+    (dict(head_dim=96), kvec.KVEC_ERR_UNSUPPORTED),
+    (dict(n_q_heads=24), kvec.KVEC_ERR_UNSUPPORTED),        # G = 3
+    (dict(n_kv_heads=32, n_q_heads=32), kvec.KVEC_ERR_UNSUPPORTED),
+])
+def test_config_validation(over, code):
+    st, _ = _ws_status(_cfg(**over))
+    assert st == code
+
+
+def test_entry_points_reject_before_launch():
+    lib = kvec.load()
+    c = _cfg().c()
+    st3 = (ctypes.c_int64 * 3)(32 * 64 * 128, 64 * 128, 128)
+    ks3 = (ctypes.c_int64 * 3)(8 * 32768 * 128, 32768 * 128, 128)
+    fake = ctypes.c_void_p(1 << 20)          # aligned, never dereferenced
+    # null outputs
+    assert lib.kvec_score(ctypes.byref(c), fake, st3, fake, ks3, None, fake, fake, fake, 1 << 40,
+                          None) == kvec.KVEC_ERR_INVALID
+    # misaligned input
+    assert lib.kvec_score(ctypes.byref(c), ctypes.c_void_p((1 << 20) + 2), st3, fake, ks3, fake,
+                          fake, fake, fake, 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    # stride not a multiple of 16 bytes
+    bad = (ctypes.c_int64 * 3)(8 * 32768 * 128, 32768 * 128, 127)
+    assert lib.kvec_score(ctypes.byref(c), fake, st3, fake, bad, fake, fake, fake, fake, 1 << 40,
+                          None) == kvec.KVEC_ERR_INVALID
+    # workspace too small
+    assert lib.kvec_score(ctypes.byref(c), fake, st3, fake, ks3, fake, fake, fake, fake, 16,
+                          None) == kvec.KVEC_ERR_WORKSPACE
+    # layer out of range
+    assert lib.kvec_select_cover(ctypes.byref(c), 32, fake, fake, fake, fake, fake, None, fake,
+                                 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    assert lib.kvec_select_cover(ctypes.byref(c), -1, fake, fake, fake, fake, fake, None, fake,
+                                 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    assert lib.kvec_select_cover(ctypes.byref(c), 0, fake, fake, fake, fake, fake, None, fake, 16,
+                                 None) == kvec.KVEC_ERR_WORKSPACE
+    assert lib.kvec_coverage(ctypes.byref(c), fake, 32, fake, None) == kvec.KVEC_ERR_INVALID
+    assert lib.kvec_compact(ctypes.byref(c), fake, ks3, None, ks3, fake, fake, fake,
+                            None) == kvec.KVEC_ERR_INVALID
+
+
+def test_status_strings():
+    for s in range(5):
+        assert isinstance(kvec.status_string(s), str) and kvec.status_string(s)
+    assert kvec.status_string(99) == "unknown status"

@@ -1,0 +1,226 @@
+"""GPU parity of libkvec against the float64 oracle, through the C ABI.
+
+Scores: max relative error <= 2e-3.  Selection on oracle scores: bit-exact
+indices, H_top and bitmaps.  Gather: byte-exact.  End to end: teacher-forced
+agreement >= 99.5% with every mismatch within tolerance of the cut.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as orc
+import synth
+from kvec_testlib import (AGREE_MIN, SCORE_RTOL, agreement, bits_to_bool, counts_before,
+                          layer_inputs, model_tensors, oracle_scores, rel_err, to_device)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _small(name, T, O, Wn, H, G, D, dtype, batch=1, B=None, layers=2, pool=7, delta=3, lam=1.0,
+           beta=0.25, hh=0.02, rope=True, seed=7):
+    B = B if B is not None else max(O + 8, T // 8)
+    return synth.Workload(name, layers, H, H * G, D, T, batch, O, Wn, B, pool, dtype, seed,
+                          rope=rope, hh_count=int(round(hh * T)), n_adjust_heads=min(delta, H),
+                          lam=lam, beta=beta)
+
+
+SCORE_CASES = [
+    _small("f32-d64-g2", 1024, 32, 64, 4, 2, 64, "f32", rope=False),
+    _small("f32-d64-g2-ragged", 301, 32, 64, 4, 2, 64, "f32", rope=False),
+    _small("bf16-d128-g4", 1000, 32, 64, 8, 4, 128, "bf16"),
+    _small("bf16-d128-g4-mixed", 777, 20, 40, 2, 4, 128, "bf16"),
+    _small("bf16-d64-g1-pad", 530, 20, 40, 3, 1, 64, "bf16"),
+    _small("bf16-d128-g4-o64", 2048, 64, 128, 8, 4, 128, "bf16", batch=2),
+    _small("bf16-d128-g8", 257, 5, 17, 2, 8, 128, "bf16"),
+    _small("bf16-d64-g2-short", 70, 16, 64, 2, 2, 64, "bf16"),
+    _small("f32-d128-g1", 200, 8, 8, 2, 1, 128, "f32"),
+    _small("bf16-d128-g4-wn-eq-o", 600, 32, 32, 4, 4, 128, "bf16"),
+]
+
+
+@pytest.mark.parametrize("w", SCORE_CASES, ids=lambda w: w.name)
+def test_score_parity(gpu_lib, w):
+    import torch
+    kv = gpu_lib
+    _say(f"[score] {w.name} T={w.seq_len} O={w.window} Wn={w.rows} H={w.n_kv_heads} G={w.group}")
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    Tc = w.candidates
+    for layer in range(min(w.n_layers, 2)):
+        qs, ks = [], []
+        for b in range(w.batch):
+            qa, ka, _ = layer_inputs(w, layer, b)
+            qs.append(to_device(qa, w))
+            ks.append(to_device(ka, w))
+        q = torch.stack(qs)
+        k = torch.stack(ks)
+        p = torch.empty((w.batch, w.n_kv_heads, Tc), dtype=torch.float32, device="cuda")
+        pe = torch.empty_like(p)
+        imp = torch.empty((w.batch, Tc), dtype=torch.float32, device="cuda")
+        kv.kvec_score(cfg, q, k, p, pe, imp, ws)
+        torch.cuda.synchronize()
+        for b in range(w.batch):
+            rp, rpe, rimp = oracle_scores(w, layer, b)
+            e = (rel_err(p[b].cpu().numpy(), rp), rel_err(pe[b].cpu().numpy(), rpe),
+                 rel_err(imp[b].cpu().numpy(), rimp))
+            _say(f"   layer {layer} seq {b}: rel err P {e[0]:.2e} P' {e[1]:.2e} I {e[2]:.2e}")
+            assert max(e) <= SCORE_RTOL, e
+
+
+SELECT_CASES = [
+    _small("sel-base", 4096, 32, 64, 8, 4, 128, "bf16", B=128, layers=4),
+    _small("sel-b2-pool5", 3000, 64, 128, 4, 4, 128, "bf16", batch=2, B=300, layers=3, pool=5),
+    _small("sel-pool1-nodelta", 1500, 16, 32, 4, 2, 64, "bf16", B=100, layers=3, pool=1, delta=0),
+    _small("sel-lam0", 1500, 16, 32, 4, 2, 64, "bf16", B=100, layers=3, lam=0.0),
+    _small("sel-beta0", 1500, 16, 32, 4, 2, 64, "bf16", B=100, layers=3, beta=0.0),
+    _small("sel-beta1", 1500, 16, 32, 4, 2, 64, "bf16", B=100, layers=3, beta=1.0),
+    _small("sel-wn-eq-o", 1500, 16, 16, 4, 2, 64, "bf16", B=100, layers=3),
+    _small("sel-ragged", 999, 7, 14, 3, 1, 64, "bf16", B=41, layers=3, pool=3),
+]
+
+
+@pytest.mark.parametrize("w", SELECT_CASES, ids=lambda w: w.name)
+def test_select_on_oracle_scores(gpu_lib, w):
+    """Selection fed the oracle's fp32 scores is bit-exact with the oracle."""
+    import torch
+    kv = gpu_lib
+    _say(f"[select] {w.name} T={w.seq_len} B={w.budget} layers={w.n_layers} batch={w.batch}")
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    T, Tc, H, B = w.seq_len, w.candidates, w.n_kv_heads, w.budget
+    W = (T + 63) // 64
+    bits = torch.zeros((w.batch, w.n_layers, W), dtype=torch.int64, device="cuda")
+    idx = torch.empty((w.batch, H, B), dtype=torch.int32, device="cuda")
+    htop = torch.empty((w.batch,), dtype=torch.int32, device="cuda")
+    prev = [[] for _ in range(w.batch)]
+    for layer in range(w.n_layers):
+        sc = [orc.score_layer(synth.to_f64(synth.queries(w, layer, b), w.dtype),
+                              synth.to_f64(synth.keys(w, layer, b), w.dtype), w.window)
+              for b in range(w.batch)]
+        p = torch.from_numpy(np.stack([s[0] for s in sc])).cuda()
+        pe = torch.from_numpy(np.stack([s[1] for s in sc])).cuda()
+        imp = torch.from_numpy(np.stack([s[2] for s in sc])).cuda()
+        kv.kvec_select_cover(cfg, layer, p, pe, imp, bits, idx, htop, ws)
+        torch.cuda.synchronize()
+        gi = idx.cpu().numpy()
+        gb = bits.cpu().numpy().view(np.uint64)
+        gh = htop.cpu().numpy()
+        for b in range(w.batch):
+            n_t = orc.counts_from_bits(prev[b]) if prev[b] else np.zeros(T, np.int64)
+            res = orc.evict_layer_from_scores(sc[b][0], sc[b][1], sc[b][2], n_t, layer, w)
+            np.testing.assert_array_equal(gi[b], res.idx, err_msg=f"layer {layer} seq {b}")
+            want_mask = sum(1 << int(h) for h in res.htop)
+            assert int(gh[b]) & 0xFFFF == want_mask, (layer, b, gh[b], res.htop)
+            np.testing.assert_array_equal(bits_to_bool(gb[b, layer], T), res.bits)
+            prev[b].append(res.bits)
+        _say(f"   layer {layer}: idx, H_top and bitmap bit-exact")
+
+
+def test_keep_everything_when_budget_covers(gpu_lib):
+    import torch
+    kv = gpu_lib
+    w = _small("keep-all", 100, 8, 16, 2, 2, 64, "bf16", B=128, layers=2)
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(max(kv.kvec_workspace_size(cfg), 256), dtype=torch.uint8, device="cuda")
+    q, k, v = model_tensors(w)
+    W = (w.seq_len + 63) // 64
+    bits = torch.zeros((1, 2, W), dtype=torch.int64, device="cuda")
+    idx = torch.empty((2, 1, 2, 128), dtype=torch.int32, device="cuda")
+    ko = torch.empty((2, 1, 2, 128, 64), dtype=k.dtype, device="cuda")
+    vo = torch.empty_like(ko)
+    kv.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
+    torch.cuda.synchronize()
+    gi = idx.cpu().numpy()
+    assert np.all(gi[:, :, :, :100] == np.arange(100))
+    assert np.all(gi[:, :, :, 100:] == -1)
+    assert np.all(ko[:, :, :, 100:].float().cpu().numpy() == 0)
+    assert torch.equal(ko[:, :, :, :100], k)
+
+
+def test_compact_bit_exact(gpu_lib):
+    import torch
+    kv = gpu_lib
+    w = _small("compact", 500, 8, 16, 3, 2, 128, "bf16", batch=2, B=64, layers=1)
+    cfg = kv.Config.from_workload(w)
+    g = torch.Generator().manual_seed(3)
+    k = torch.randn((2, 3, 500, 128), generator=g).to(torch.bfloat16).cuda()
+    v = torch.randn((2, 3, 500, 128), generator=g).to(torch.bfloat16).cuda()
+    idx = torch.randint(-1, 500, (2, 3, 64), generator=g, dtype=torch.int32).cuda()
+    ko = torch.empty((2, 3, 64, 128), dtype=torch.bfloat16, device="cuda")
+    vo = torch.empty_like(ko)
+    kv.kvec_compact(cfg, k, v, idx, ko, vo)
+    torch.cuda.synchronize()
+    ki = idx.cpu().numpy()
+    kn, vn = k.cpu().view(torch.int16).numpy(), v.cpu().view(torch.int16).numpy()
+    want_k = np.stack([orc.gather_rows(kn[b], ki[b]) for b in range(2)])
+    want_v = np.stack([orc.gather_rows(vn[b], ki[b]) for b in range(2)])
+    np.testing.assert_array_equal(ko.cpu().view(torch.int16).numpy(), want_k)
+    np.testing.assert_array_equal(vo.cpu().view(torch.int16).numpy(), want_v)
+
+
+def _e2e(kv, w, check_layers=None):
+    """Run the whole-model driver and check sampled layers teacher-forced."""
+    import torch
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    _say(f"[e2e] {w.name}: generating inputs")
+    q, k, v = model_tensors(w)
+    L, H, B, T, d = w.n_layers, w.n_kv_heads, w.budget, w.seq_len, w.head_dim
+    W = (T + 63) // 64
+    bits = torch.empty((w.batch, L, W), dtype=torch.int64, device="cuda")
+    idx = torch.empty((L, w.batch, H, B), dtype=torch.int32, device="cuda")
+    ko = torch.empty((L, w.batch, H, B, d), dtype=k.dtype, device="cuda")
+    vo = torch.empty_like(ko)
+    kv.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
+    torch.cuda.synchronize()
+    _say(f"[e2e] {w.name}: device step done")
+    gi = idx.cpu().numpy()
+    gb = bits.cpu().numpy().view(np.uint64)
+    M = B - w.window
+    kp = orc.preserve_count(B, w.window, w.beta)
+    layers = range(L) if check_layers is None else check_layers
+    tot_m = tot = 0
+    for l in layers:
+        for b in range(w.batch):
+            p, pe, imp = oracle_scores(w, l, b)
+            n_t = counts_before(gb[b], l, T)
+            res = orc.evict_layer_from_scores(orc.to_f32(p), orc.to_f32(pe), orc.to_f32(imp),
+                                              n_t, l, w)
+            m, t, bad = agreement(gi[l, b], res, M, kp)
+            tot_m += m
+            tot += t
+            assert not bad, f"layer {l} seq {b}: mismatches away from the cut {bad[:5]}"
+            # the window, the layout and the bitmap row
+            assert np.all(gi[l, b, :, M:] == np.arange(T - w.window, T))
+            assert np.all(np.diff(gi[l, b, :, :M], axis=1) > 0)
+            np.testing.assert_array_equal(bits_to_bool(gb[b, l], T),
+                                          orc.layer_bits(gi[l, b], T))
+            # gather is byte-exact for the GPU's own indices
+            kk = k[l, b].cpu().view(torch.int16).numpy()
+            np.testing.assert_array_equal(ko[l, b].cpu().view(torch.int16).numpy(),
+                                          orc.gather_rows(kk, gi[l, b]))
+        _say(f"   layer {l}: agreement so far {tot_m / tot:.5f}")
+    assert tot_m / tot >= AGREE_MIN
+    # coverage equals the union of the kept index sets
+    cnt = torch.empty((w.batch,), dtype=torch.int64, device="cuda")
+    kv.kvec_coverage(cfg, bits, L - 1, cnt)
+    torch.cuda.synchronize()
+    for b in range(w.batch):
+        u = set()
+        for l in range(L):
+            u |= set(gi[l, b].ravel().tolist())
+        u.discard(-1)
+        assert int(cnt[b]) == len(u)
+
+
+def test_e2e_tiny_fp32(gpu_lib):
+    _e2e(gpu_lib, synth.workload(0))
+
+
+def test_e2e_small_bf16(gpu_lib):
+    _e2e(gpu_lib, _small("e2e-small", 2500, 32, 64, 8, 4, 128, "bf16", B=200, layers=6))
