@@ -128,7 +128,8 @@ def main():
     print("[bench] inputs resident; warming up", file=sys.stderr, flush=True)
 
     hip = _hip()
-    evs = [_events(hip, 4 * L) for _ in range(args.steps)]
+    n_ev = kvec.kvec_profile_points(cfg)
+    evs = [_events(hip, n_ev) for _ in range(args.steps)]
     for _ in range(args.warmup):
         kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
     torch.cuda.synchronize()
@@ -140,28 +141,27 @@ def main():
     ms_step = wall * 1e3 / args.steps
     print(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms", file=sys.stderr, flush=True)
 
-    # Per-kernel durations of the two score passes (HIP events on the library's stream).
-    p1 = p2 = 0.0
+    # Duration of each fused launch of the step (HIP events on the library's
+    # stream).  In the steady state a launch does one layer's worth of every
+    # stage: pass 1 of layer j, pass 2 of j-1, pooling of j-2, candidates of
+    # j-3, the coverage selection of j-4 and the gather of j-5.
+    durs = []
     for s in range(args.steps):
         e = evs[s]
-        for l in range(L):
-            p1 += _elapsed(hip, e[4 * l], e[4 * l + 1])
-            p2 += _elapsed(hip, e[4 * l + 2], e[4 * l + 3])
-    n = args.steps * L
-    p1, p2 = p1 / n, p2 / n
+        durs += [_elapsed(hip, e[i], e[i + 1]) for i in range(n_ev - 1)]
+    n_launch = n_ev - 1
+    avg_ms = sum(durs) / len(durs)
     es = 2 if w.dtype == "bf16" else 4
-    Tc = T - w.window
-    k_bytes_p1 = b * H * T * d * es + b * HQ * w.rows * d * es
-    k_bytes_p2 = b * H * Tc * d * es + b * HQ * w.rows * d * es
-    if p2 >= p1:
-        kern, dur, byts = "score pass 2 (probabilities, window sums, head max)", p2, k_bytes_p2
-    else:
-        kern, dur, byts = "score pass 1 (row normalisers)", p1, k_bytes_p1
-    achieved = byts / (dur * 1e-3) / 1e9
+    # algorithmic bytes of the whole step: K read once, the Q window, the gather
+    # (read and write of the kept K and V rows)
+    step_bytes = L * b * (H * T * d * es + HQ * w.rows * d * es + 4 * H * B * d * es)
+    per_launch = step_bytes / n_launch
+    achieved = per_launch / (avg_ms * 1e-3) / 1e9
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kern,
-            "avg_launch_us": round(dur * 1e3, 2),
-            "pass1_us": round(p1 * 1e3, 2), "pass2_us": round(p2 * 1e3, 2)}
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": "step_kernel (fused pipeline launch)", "launches_per_step": n_launch,
+            "avg_launch_us": round(avg_ms * 1e3, 2),
+            "algorithmic_bytes_per_launch": int(per_launch)}
 
     cpu = None
     if not args.no_cpu_baseline:

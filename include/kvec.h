@@ -60,7 +60,7 @@ extern "C" {
 typedef enum kvec_status {
   KVEC_OK = 0,
   KVEC_ERR_INVALID = 1,      /* bad argument, shape, alignment or null pointer */
-  KVEC_ERR_UNSUPPORTED = 2,  /* valid but not implemented (head_dim, group size) */
+  KVEC_ERR_UNSUPPORTED = 2,  /* valid but not implemented (head count, head_dim, group size) */
   KVEC_ERR_WORKSPACE = 3,    /* workspace smaller than kvec_workspace_size() */
   KVEC_ERR_DEVICE = 4        /* a HIP launch or runtime call failed */
 } kvec_status;
@@ -74,14 +74,14 @@ typedef enum kvec_dtype {
 typedef struct kvec_config {
   int32_t batch;          /* independent sequences, >= 1 */
   int32_t n_layers;       /* L, >= 1 (rows of the coverage bitmap) */
-  int32_t n_kv_heads;     /* H, 1..16 */
+  int32_t n_kv_heads;     /* H in {1, 2, 4, 8} */
   int32_t n_q_heads;      /* multiple of H; G = n_q_heads / H in {1, 2, 4, 8} */
   int32_t head_dim;       /* d in {64, 128} */
-  int32_t seq_len;        /* T, prefix length including the window, >= 1 */
+  int32_t seq_len;        /* T, prefix length including the window, 1..262144 */
   int32_t window;         /* O, 1 <= O <= T */
   int32_t window_ext;     /* O' >= O (clamped to T); O' == O turns cross-head off */
   int32_t budget;         /* B per KV head including the window, B >= O */
-  int32_t pool_kernel;    /* odd, >= 1: max-pool width along t (1 = none) */
+  int32_t pool_kernel;    /* odd, 1..63: max-pool width along t (1 = none) */
   int32_t n_adjust_heads; /* delta, 0..H: heads switched to the O' score */
   float lambda;           /* >= 0: cross-layer bonus weight (0 = off) */
   float beta;             /* in [0, 1]: preserve K = min(floor(beta*B), B-O) per head */
@@ -113,10 +113,12 @@ kvec_status kvec_score(const kvec_config* cfg,
  *   layer       0-based index l; coverage uses n_t/(l+1).
  *   p_raw, p_ext_raw, imp  device fp32, as written by kvec_score.
  *   cover_bits  device uint64 [batch][n_layers][ceil(T/64)]: bit (l', t) set
- *               when layer l' kept token t in at least one head.  Read for
- *               layers < layer (n_t = number of those layers holding t),
- *               written (atomic OR) for `layer`.  The caller zeroes the whole
- *               bitmap before layer 0 and calls layers in increasing order.
+ *               when layer l' kept token t in at least one head.  Rows
+ *               l' < layer are read (n_t = number of those rows holding t);
+ *               row `layer` is overwritten (cleared, then the kept tokens and
+ *               the window set); rows > layer are not touched.  Layers are
+ *               called in increasing order, so that rows 0..layer-1 hold this
+ *               problem's earlier selections (layer 0 reads nothing).
  *   idx         device out, int32 [batch][H][B]: the B-O prefix picks in
  *               ascending order, then the window T-O..T-1.  If T <= B every
  *               token is kept: 0..T-1, remaining slots -1.
@@ -145,15 +147,15 @@ kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer,
                              uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
                              void* ws, size_t ws_bytes, hipStream_t stream);
 
-/* The whole prefill eviction step: every layer in order 0..L-1.
+/* The whole prefill eviction step: every layer, the selection in order 0..L-1.
  *   q_win, k, v  device, strides {layer, batch, head, row/t}.
- *   cover_bits   device uint64 [batch][L][ceil(T/64)]; zeroed by this call.
+ *   cover_bits   device uint64 [batch][L][ceil(T/64)]; every row is written.
  *   idx          device out int32 [L][batch][H][B].
  *   k_out, v_out device out, contiguous [L][batch][H][B][d].
- *   events       nullable; else 4*L caller-created HIP events recorded on
- *                `stream` for profiling: for layer l, events[4l+0..1]
- *                bracket the score pass that forms the row normalisers and
- *                events[4l+2..3] the pass that forms the scores. */
+ *   events       nullable; else kvec_profile_points(cfg) caller-created HIP
+ *                events.  The step runs as a sequence of fused launches;
+ *                events[i] is recorded on `stream` before launch i and the
+ *                last event after the final launch (profiling only). */
 kvec_status kvec_evict_model(const kvec_config* cfg,
                              const void* q_win, const int64_t q_strides[4],
                              const void* k, const int64_t k_strides[4],
@@ -161,6 +163,10 @@ kvec_status kvec_evict_model(const kvec_config* cfg,
                              uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
                              void* ws, size_t ws_bytes, hipStream_t stream,
                              hipEvent_t* events);
+
+/* Number of events kvec_evict_model records when given an event array
+ * (n_layers + 7; 0 when T <= B), or -1 for an invalid configuration. */
+int32_t kvec_profile_points(const kvec_config* cfg);
 
 /* Coverage C (Sec. 3.2) per sequence over layers 0..upto_layer:
  * count_per_seq[b] = popcount of the OR of those layers' bitmaps.

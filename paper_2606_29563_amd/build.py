@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkvec.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["kvec_api.hip", "kvec_score.hip", "kvec_select.hip", "kvec_compact.hip"]
+SOURCES = ["kvec_api.hip", "kvec_pipeline.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -1,4 +1,4 @@
-// C ABI of libkvec: argument validation, workspace layout and launch order.
+// C ABI of libkvec: argument validation, workspace layout and call dispatch.
 // Everything here is host code; validation never touches the device.
 #include <math.h>
 #include <string.h>
@@ -7,7 +7,8 @@
 
 namespace kvec {
 
-int row_blocks_per_tile(int G);  // kvec_score.hip
+constexpr size_t kLdsMax = 163840;  // bytes of LDS per work-group on gfx950
+constexpr size_t kLdsStatic = 1024; // reserve for the tasks' static shared variables
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -16,7 +17,7 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   if (c->batch < 1 || c->n_layers < 1 || c->n_layers > 255) return KVEC_ERR_INVALID;
   if (c->n_kv_heads < 1 || c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads != 0)
     return KVEC_ERR_INVALID;
-  if (c->seq_len < 1 || c->seq_len > (1 << 28)) return KVEC_ERR_INVALID;
+  if (c->seq_len < 1) return KVEC_ERR_INVALID;
   if (c->window < 1 || c->window > c->seq_len) return KVEC_ERR_INVALID;
   if (c->window_ext < c->window) return KVEC_ERR_INVALID;
   if (c->budget < c->window) return KVEC_ERR_INVALID;
@@ -26,16 +27,19 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   if (!(c->beta >= 0.f && c->beta <= 1.f)) return KVEC_ERR_INVALID;
   if (c->dtype != KVEC_BF16 && c->dtype != KVEC_F32) return KVEC_ERR_INVALID;
   if (c->head_dim < 1) return KVEC_ERR_INVALID;
-  const int G = c->n_q_heads / c->n_kv_heads;
-  if (c->n_kv_heads > 16) return KVEC_ERR_UNSUPPORTED;
+  const int H = c->n_kv_heads, G = c->n_q_heads / c->n_kv_heads;
+  if (H != 1 && H != 2 && H != 4 && H != 8) return KVEC_ERR_UNSUPPORTED;
   if (G != 1 && G != 2 && G != 4 && G != 8) return KVEC_ERR_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return KVEC_ERR_UNSUPPORTED;
-  if ((int64_t)c->budget * c->n_kv_heads > (1 << 28)) return KVEC_ERR_UNSUPPORTED;
+  if (c->seq_len > (1 << 18)) return KVEC_ERR_UNSUPPORTED;
+  if (c->pool_kernel > 63) return KVEC_ERR_UNSUPPORTED;
+  if ((int64_t)c->budget * H > (1 << 26)) return KVEC_ERR_UNSUPPORTED;
 
-  Geometry& x = *g;
+  Problem& x = g->p;
+  memset(&x, 0, sizeof(x));
   x.batch = c->batch;
-  x.layers = c->n_layers;
-  x.H = c->n_kv_heads;
+  x.L = c->n_layers;
+  x.H = H;
   x.HQ = c->n_q_heads;
   x.G = G;
   x.D = c->head_dim;
@@ -44,53 +48,86 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   x.Wn = c->window_ext < c->seq_len ? c->window_ext : c->seq_len;
   x.Tc = c->seq_len - c->window;
   x.B = c->budget;
-  x.pool = c->pool_kernel;
-  x.delta = c->n_adjust_heads;
-  x.lam = c->lambda;
-  x.beta = c->beta;
-  x.dtype = c->dtype;
   x.M = c->budget - c->window;
   const double kp = floor((double)c->beta * (double)c->budget);
   x.Kp = (int)(kp < (double)x.M ? kp : (double)x.M);
-  x.RB = row_blocks_per_tile(G);
-  x.WR = 16 * x.RB;
+  x.pool = c->pool_kernel;
+  x.delta_eff = x.Wn > x.O ? c->n_adjust_heads : 0;
+  x.lam = c->lambda;
+  x.sc = (float)(1.4426950408889634 / sqrt((double)x.D));
+  x.inv_go = (float)(1.0 / ((double)G * x.O));
+  x.inv_gwn = (float)(1.0 / ((double)G * x.Wn));
+  x.WR = 16 * row_blocks_per_tile(G);
   x.n_rt = (x.Wn + x.WR - 1) / x.WR;
   x.n_rt_base = (x.O + x.WR - 1) / x.WR;
-  x.n_kt1 = (x.T + kTilePass1 - 1) / kTilePass1;
-  x.n_kt2 = (x.Tc + kTilePass2 - 1) / kTilePass2;
+  const int tpw = 8 / H;
+  x.n_rtg = (x.n_rt + tpw - 1) / tpw;
+  x.n_kt1 = (x.T + kTile1 - 1) / kTile1;
+  x.n_kt2 = (x.Tc + kTile2 - 1) / kTile2;
   x.SK = 64;
-  while (x.SK > 16 && ((size_t)x.H * x.WR * x.SK + 64 * x.H) * 4 > 65536) x.SK /= 2;
-  x.n_pool_blk = (x.Tc + kPoolBlock - 1) / kPoolBlock;
+  while (x.SK > 16 && ((size_t)tpw * ((size_t)H * x.WR * x.SK + 64 * H + 2 * H * kTile2 + kTile2)) * 4 >
+                          98304)
+    x.SK /= 2;
+  x.n_pool = (x.Tc + kPoolChunk - 1) / kPoolChunk;
+  x.n_prep = (x.Tc + kPrepChunk - 1) / kPrepChunk;
   x.words = (x.T + 63) / 64;
   x.esize = c->dtype == KVEC_BF16 ? 2 : 4;
-  x.keep_all = x.T <= x.B;
+  const int64_t chunks = (int64_t)H * x.B * (x.D * x.esize / 16);
+  x.n_gather = (int)((chunks + 4 * kThreads - 1) / (4 * kThreads));
+  // selection task LDS: 2048-bin histogram, 32 ints, member offsets, then
+  // four 4-byte arrays per member
+  const size_t sel_fixed = 2048 * 4 + 32 * 4 + (size_t)((x.n_prep + 1 + 3) & ~3) * 4;
+  x.mcap = (int)(((kLdsMax - kLdsStatic - sel_fixed) / 16) & ~(size_t)63);
+  g->keep_all = x.T <= x.B;
   return KVEC_OK;
 }
 
 Workspace make_workspace(const Geometry& g) {
+  const Problem& P = g.p;
   Workspace w;
+  memset(&w, 0, sizeof(w));
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
     off += align256(bytes);
     return at;
   };
-  const size_t bt = (size_t)g.batch, tc = (size_t)(g.Tc > 0 ? g.Tc : 0);
-  w.lse_part = take(bt * g.HQ * g.Wn * g.n_kt1 * 8);
-  w.lse2 = take(bt * g.HQ * g.Wn * 4);
-  w.psum_base = take(bt * g.n_rt * g.H * tc * 4);
-  w.psum_all = take(bt * g.n_rt * g.H * tc * 4);
-  w.ipart = take(bt * g.n_rt * tc * 4);
-  w.p_raw = take(bt * g.H * tc * 4);
-  w.p_ext = take(bt * g.H * tc * 4);
+  const size_t bt = (size_t)P.batch, tc = (size_t)(P.Tc > 0 ? P.Tc : 0);
+  // one ring slot
+  w.lse_part = take(bt * P.HQ * P.Wn * P.n_kt1 * 8);
+  w.lse2 = take(bt * P.HQ * P.Wn * 4);
+  w.psum_base = take(bt * P.n_rt * P.H * tc * 4);
+  w.psum_all = take(bt * P.n_rt * P.H * tc * 4);
+  w.ipart = take(bt * P.n_rt * tc * 4);
   w.imp = take(bt * tc * 4);
-  w.pooled = take(bt * g.H * tc * 4);
-  w.pooled_ext = take(bt * g.H * tc * 4);
-  w.stats = take(bt * g.H * g.n_pool_blk * 16);
-  w.use_ext = take(bt * g.H * 4);
-  w.keep = take(bt * g.H * ((tc + 31) / 32) * 4);
-  w.keys = take(bt * g.H * tc * 4);
+  w.pooled = take(bt * P.H * tc * 4);
+  w.pooled_ext = take(bt * P.H * tc * 4);
+  w.stats = take(bt * P.H * P.n_pool * 16);
+  w.hist = take(bt * 2 * P.H * kHistBins * 4);
+  w.mem_t = take(bt * P.H * tc * 4);
+  w.mem_ps = take(bt * P.H * tc * 4);
+  w.mem_i = take(bt * P.H * tc * 4);
+  w.mem_n = take(bt * P.H * P.n_prep * 4);
+  w.slot_bytes = off;
+  off = w.slot_bytes * kRing;
+  w.counts_stride = align256(bt * P.T);
+  w.counts = take(2 * w.counts_stride);
+  w.spill_stride = align256(bt * P.H * tc * 4);
+  w.spill = take(4 * w.spill_stride);
   w.total = off;
+  // dynamic LDS: the largest task
+  const int tpw = 8 / P.H;
+  const size_t lds_p2 =
+      (size_t)tpw * ((size_t)P.H * P.WR * P.SK + 64 * P.H + 2 * P.H * kTile2 + kTile2) * 4;
+  const size_t lds_pool = (size_t)(2 * (kPoolChunk + 64) + 2 * kHistBins) * 4 + 16 * 8;
+  const size_t lds_prep = 256;
+  const size_t lds_sel = 2048 * 4 + 32 * 4 + (size_t)((P.n_prep + 1 + 3) & ~3) * 4 +
+                         (size_t)16 * P.mcap;
+  size_t lds = lds_p2;
+  if (lds_pool > lds) lds = lds_pool;
+  if (lds_prep > lds) lds = lds_prep;
+  if (lds_sel > lds) lds = lds_sel;
+  w.lds_bytes = (lds + 15) & ~(size_t)15;
   return w;
 }
 
@@ -118,6 +155,13 @@ kvec_status check_ws(const Geometry& g, void* ws, size_t ws_bytes) {
   return KVEC_OK;
 }
 
+void strides4(int64_t out[4], const int64_t* s3) {
+  out[0] = 0;
+  out[1] = s3[0];
+  out[2] = s3[1];
+  out[3] = s3[2];
+}
+
 }  // namespace
 
 extern "C" {
@@ -137,14 +181,14 @@ kvec_status kvec_score(const kvec_config* cfg, const void* q_win, const int64_t 
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
-  if (g.Tc < 1) return KVEC_ERR_INVALID;
-  if (!aligned16(q_win) || !aligned16(k) || !strides_ok(q_strides, 3, g.esize) ||
-      !strides_ok(k_strides, 3, g.esize) || !p_raw || !p_ext_raw || !imp)
+  if (g.p.Tc < 1) return KVEC_ERR_INVALID;
+  if (!aligned16(q_win) || !aligned16(k) || !strides_ok(q_strides, 3, g.p.esize) ||
+      !strides_ok(k_strides, 3, g.p.esize) || !p_raw || !p_ext_raw || !imp)
     return KVEC_ERR_INVALID;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
-  return dev(launch_score(g, q_win, q_strides, k, k_strides, p_raw, p_ext_raw, imp,
-                          static_cast<char*>(ws), w, stream, nullptr));
+  return dev(run_score(g, q_win, q_strides, k, k_strides, p_raw, p_ext_raw, imp,
+                       static_cast<char*>(ws), w, stream));
 }
 
 kvec_status kvec_select_cover(const kvec_config* cfg, int32_t layer, const float* p_raw,
@@ -154,13 +198,13 @@ kvec_status kvec_select_cover(const kvec_config* cfg, int32_t layer, const float
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
-  if (layer < 0 || layer >= g.layers || !cover_bits || !idx) return KVEC_ERR_INVALID;
-  if (g.keep_all) return dev(launch_keep_all(g, layer, cover_bits, idx, stream));
+  if (layer < 0 || layer >= g.p.L || !cover_bits || !idx) return KVEC_ERR_INVALID;
+  if (g.keep_all) return dev(run_keep_all(g, layer, cover_bits, idx, stream));
   if (!p_raw || !p_ext_raw || !imp) return KVEC_ERR_INVALID;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
-  return dev(launch_select(g, layer, p_raw, p_ext_raw, imp, cover_bits, idx, htop_mask,
-                           static_cast<char*>(ws), w, stream));
+  return dev(run_select(g, layer, p_raw, p_ext_raw, imp, cover_bits, idx, htop_mask,
+                        static_cast<char*>(ws), w, stream));
 }
 
 kvec_status kvec_compact(const kvec_config* cfg, const void* k, const int64_t k_strides[3],
@@ -169,12 +213,19 @@ kvec_status kvec_compact(const kvec_config* cfg, const void* k, const int64_t k_
   Geometry g;
   const kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
-  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 3, g.esize) ||
-      !strides_ok(v_strides, 3, g.esize) || !idx || !aligned16(k_out) || !aligned16(v_out))
+  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 3, g.p.esize) ||
+      !strides_ok(v_strides, 3, g.p.esize) || !idx || !aligned16(k_out) || !aligned16(v_out))
     return KVEC_ERR_INVALID;
-  const int64_t ks[4] = {0, k_strides[0], k_strides[1], k_strides[2]};
-  const int64_t vs[4] = {0, v_strides[0], v_strides[1], v_strides[2]};
-  return dev(launch_compact(g, 1, k, ks, v, vs, idx, k_out, v_out, stream));
+  ModelIO m;
+  memset(&m, 0, sizeof(m));
+  m.k = k;
+  m.v = v;
+  strides4(m.ks, k_strides);
+  strides4(m.vs, v_strides);
+  m.idx = const_cast<int32_t*>(idx);
+  m.k_out = k_out;
+  m.v_out = v_out;
+  return dev(run_compact(g, 1, m, stream));
 }
 
 kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* q_win,
@@ -185,30 +236,32 @@ kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* 
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
-  if (layer < 0 || layer >= g.layers || !cover_bits || !idx) return KVEC_ERR_INVALID;
-  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 3, g.esize) ||
-      !strides_ok(v_strides, 3, g.esize) || !aligned16(k_out) || !aligned16(v_out))
+  if (layer < 0 || layer >= g.p.L || !cover_bits || !idx) return KVEC_ERR_INVALID;
+  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 3, g.p.esize) ||
+      !strides_ok(v_strides, 3, g.p.esize) || !aligned16(k_out) || !aligned16(v_out))
     return KVEC_ERR_INVALID;
-  if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 3, g.esize)))
+  if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 3, g.p.esize)))
     return KVEC_ERR_INVALID;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
-  char* wsb = static_cast<char*>(ws);
-  hipError_t e;
+  ModelIO m;
+  memset(&m, 0, sizeof(m));
+  m.q = q_win;
+  m.k = k;
+  m.v = v;
+  if (q_strides) strides4(m.qs, q_strides);
+  strides4(m.ks, k_strides);
+  strides4(m.vs, v_strides);
+  m.bits = cover_bits;
+  m.idx = idx;
+  m.k_out = k_out;
+  m.v_out = v_out;
   if (g.keep_all) {
-    e = launch_keep_all(g, layer, cover_bits, idx, stream);
-  } else {
-    float* p_raw = reinterpret_cast<float*>(wsb + w.p_raw);
-    float* p_ext = reinterpret_cast<float*>(wsb + w.p_ext);
-    float* imp = reinterpret_cast<float*>(wsb + w.imp);
-    e = launch_score(g, q_win, q_strides, k, k_strides, p_raw, p_ext, imp, wsb, w, stream, nullptr);
-    if (e == hipSuccess)
-      e = launch_select(g, layer, p_raw, p_ext, imp, cover_bits, idx, nullptr, wsb, w, stream);
+    const hipError_t e = run_keep_all(g, layer, cover_bits, idx, stream);
+    if (e != hipSuccess) return KVEC_ERR_DEVICE;
+    return dev(run_compact(g, 1, m, stream));
   }
-  if (e != hipSuccess) return KVEC_ERR_DEVICE;
-  const int64_t ks[4] = {0, k_strides[0], k_strides[1], k_strides[2]};
-  const int64_t vs[4] = {0, v_strides[0], v_strides[1], v_strides[2]};
-  return dev(launch_compact(g, 1, k, ks, v, vs, idx, k_out, v_out, stream));
+  return dev(run_evict_layer(g, layer, m, static_cast<char*>(ws), w, stream));
 }
 
 kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const int64_t q_strides[4],
@@ -220,35 +273,36 @@ kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const in
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
   if (!cover_bits || !idx) return KVEC_ERR_INVALID;
-  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 4, g.esize) ||
-      !strides_ok(v_strides, 4, g.esize) || !aligned16(k_out) || !aligned16(v_out))
+  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 4, g.p.esize) ||
+      !strides_ok(v_strides, 4, g.p.esize) || !aligned16(k_out) || !aligned16(v_out))
     return KVEC_ERR_INVALID;
-  if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 4, g.esize)))
+  if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 4, g.p.esize)))
     return KVEC_ERR_INVALID;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
-  char* wsb = static_cast<char*>(ws);
-  hipError_t e = launch_zero_bits(g, cover_bits, stream);
-  float* p_raw = reinterpret_cast<float*>(wsb + w.p_raw);
-  float* p_ext = reinterpret_cast<float*>(wsb + w.p_ext);
-  float* imp = reinterpret_cast<float*>(wsb + w.imp);
-  const int64_t per_layer_idx = (int64_t)g.batch * g.H * g.B;
-  for (int l = 0; l < g.layers && e == hipSuccess; ++l) {
-    int32_t* idx_l = idx + l * per_layer_idx;
-    if (g.keep_all) {
-      e = launch_keep_all(g, l, cover_bits, idx_l, stream);
-      continue;
-    }
-    const char* ql = static_cast<const char*>(q_win) + (int64_t)l * q_strides[0] * g.esize;
-    const char* kl = static_cast<const char*>(k) + (int64_t)l * k_strides[0] * g.esize;
-    e = launch_score(g, ql, q_strides + 1, kl, k_strides + 1, p_raw, p_ext, imp, wsb, w, stream,
-                     events ? events + 4 * l : nullptr);
-    if (e == hipSuccess)
-      e = launch_select(g, l, p_raw, p_ext, imp, cover_bits, idx_l, nullptr, wsb, w, stream);
+  ModelIO m;
+  memset(&m, 0, sizeof(m));
+  m.q = q_win;
+  m.k = k;
+  m.v = v;
+  for (int i = 0; i < 4; ++i) {
+    m.qs[i] = q_strides ? q_strides[i] : 0;
+    m.ks[i] = k_strides[i];
+    m.vs[i] = v_strides[i];
   }
-  if (e == hipSuccess)
-    e = launch_compact(g, g.layers, k, k_strides, v, v_strides, idx, k_out, v_out, stream);
-  return dev(e);
+  m.bits = cover_bits;
+  m.idx = idx;
+  m.k_out = k_out;
+  m.v_out = v_out;
+  if (g.keep_all) {
+    for (int l = 0; l < g.p.L; ++l) {
+      const hipError_t e = run_keep_all(g, l, cover_bits, idx + (int64_t)l * g.p.batch * g.p.H * g.p.B,
+                                        stream);
+      if (e != hipSuccess) return KVEC_ERR_DEVICE;
+    }
+    return dev(run_compact(g, g.p.L, m, stream));
+  }
+  return dev(run_model(g, m, static_cast<char*>(ws), w, stream, events));
 }
 
 kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, int32_t upto_layer,
@@ -256,9 +310,15 @@ kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, in
   Geometry g;
   const kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
-  if (!cover_bits || !count_per_seq || upto_layer < 0 || upto_layer >= g.layers)
+  if (!cover_bits || !count_per_seq || upto_layer < 0 || upto_layer >= g.p.L)
     return KVEC_ERR_INVALID;
-  return dev(launch_coverage(g, cover_bits, upto_layer, count_per_seq, stream));
+  return dev(run_coverage(g, cover_bits, upto_layer, count_per_seq, stream));
+}
+
+int32_t kvec_profile_points(const kvec_config* cfg) {
+  Geometry g;
+  if (make_geometry(cfg, &g) != KVEC_OK) return -1;
+  return g.keep_all ? 0 : g.p.L + 7;
 }
 
 const char* kvec_status_string(kvec_status s) {

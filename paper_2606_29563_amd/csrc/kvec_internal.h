@@ -9,73 +9,84 @@
 
 namespace kvec {
 
-constexpr int kWave = 64;
+constexpr int kThreads = 512;  // every work-group of the step kernel: 8 waves
+constexpr int kRing = 6;       // layers in flight in the software pipeline
 
-// Key-tile sizes of the two window-score passes (multiples of 16).
-constexpr int kTilePass1 = 512;
-constexpr int kTilePass2 = 256;
-// Tokens per block of the pooling/statistics kernel.
-constexpr int kPoolBlock = 256;
-// Threads of the per-head selection kernels.
-constexpr int kSelectThreads = 1024;
+constexpr int kTile1 = 512;       // keys per pass-1 work-group
+constexpr int kTile2 = 256;       // keys per pass-2 work-group
+constexpr int kPoolChunk = 1024;  // tokens per pool task
+constexpr int kPrepChunk = 1024;  // tokens per prep task
+constexpr int kHistBits = 12;     // selection histograms over the top 12 key bits
+constexpr int kHistBins = 1 << kHistBits;
 
-// Derived geometry of one problem.
-struct Geometry {
-  int batch, layers, H, HQ, G, D, T, O, Wn, Tc, B, pool, delta;
-  float lam, beta;
-  int dtype;
-  int Kp;        // preserved tokens per head
-  int M;         // prefix picks per head, B - O
-  int RB;        // 16-row window blocks per row tile
-  int WR;        // window rows per row tile, 16 * RB
-  int n_rt;      // row tiles covering the Wn window rows
-  int n_rt_base; // row tiles (from the newest) holding base-window rows
-  int n_kt1;     // key tiles of pass 1 over [0, T)
-  int n_kt2;     // key tiles of pass 2 over [0, Tc)
-  int SK;        // keys per importance exchange in pass 2
-  int n_pool_blk;
-  int words;     // ceil(T / 64)
-  int esize;     // bytes per element of Q/K/V
-  bool keep_all; // T <= B
+// Row tiling of the score passes: a wave computes NB = G * RB blocks of 16
+// query rows, i.e. RB 16-row blocks of the window for each of the G query
+// heads of its KV head.
+template <int G>
+struct Tiling {
+  static constexpr int RB = G >= 4 ? 1 : 4 / G;
+  static constexpr int NB = G * RB;
+  static constexpr int WR = 16 * RB;  // window rows per row tile
 };
 
-// Workspace carve-up (byte offsets, each 256-byte aligned).
+inline int row_blocks_per_tile(int G) { return G >= 4 ? 1 : 4 / G; }
+
+// Problem geometry visible to device code.
+struct Problem {
+  int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;
+  float lam, sc, inv_go, inv_gwn;
+  int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK;
+  int n_pool, n_prep, words;
+  int esize;
+  int n_gather;  // gather work-groups per (layer, sequence)
+  int mcap;      // selection members per head held in LDS
+};
+
+struct Geometry {
+  Problem p;
+  bool keep_all;  // T <= B: every token is kept
+};
+
+// Byte offsets of one ring slot (one layer in flight) and of the shared areas.
 struct Workspace {
-  size_t lse_part;   // float2 [batch][HQ][Wn][n_kt1]
-  size_t lse2;       // float  [batch][HQ][Wn]
-  size_t psum_base;  // float  [batch][n_rt][H][Tc]
-  size_t psum_all;   // float  [batch][n_rt][H][Tc]
-  size_t ipart;      // float  [batch][n_rt][Tc]
-  size_t p_raw;      // float  [batch][H][Tc]   (evict paths only)
-  size_t p_ext;      // float  [batch][H][Tc]
-  size_t imp;        // float  [batch][Tc]
-  size_t pooled;     // float  [batch][H][Tc]
-  size_t pooled_ext; // float  [batch][H][Tc]
-  size_t stats;      // double2 [batch][H][n_pool_blk]
-  size_t use_ext;    // int32  [batch][H]
-  size_t keep;       // uint32 [batch][H][ceil(Tc/32)]
-  size_t keys;       // uint32 [batch][H][Tc]
+  size_t lse_part, lse2, psum_base, psum_all, ipart, imp, pooled, pooled_ext, stats, hist, mem_t,
+      mem_ps, mem_i, mem_n;
+  size_t slot_bytes;
+  size_t counts, counts_stride;  // two uint8 [b][T] count buffers (layer parity)
+  size_t spill, spill_stride;    // four [b][H][Tc] member arrays
+  size_t lds_bytes;
   size_t total;
 };
 
 kvec_status make_geometry(const kvec_config* cfg, Geometry* g);
 Workspace make_workspace(const Geometry& g);
 
-// Launchers (return hipSuccess or the launch error).
-hipError_t launch_score(const Geometry& g, const void* q, const int64_t qs[3], const void* k,
-                        const int64_t ks[3], float* p_raw, float* p_ext, float* imp, char* ws,
-                        const Workspace& w, hipStream_t s, hipEvent_t* ev);
-hipError_t launch_select(const Geometry& g, int layer, const float* p_raw, const float* p_ext,
-                         const float* imp, uint64_t* bits, int32_t* idx, uint32_t* htop_mask,
-                         char* ws, const Workspace& w, hipStream_t s);
-hipError_t launch_keep_all(const Geometry& g, int layer, uint64_t* bits, int32_t* idx,
-                           hipStream_t s);
-hipError_t launch_compact(const Geometry& g, int n_layers, const void* k, const int64_t ks[4],
-                          const void* v, const int64_t vs[4], const int32_t* idx, void* k_out,
-                          void* v_out, hipStream_t s);
-hipError_t launch_coverage(const Geometry& g, const uint64_t* bits, int upto, int64_t* count,
-                           hipStream_t s);
-hipError_t launch_zero_bits(const Geometry& g, uint64_t* bits, hipStream_t s);
+// Host launchers (kvec_pipeline.hip).
+struct ModelIO {
+  const void* q;          // [layer][b][HQ][Wn][d] with element strides qs
+  const void* k;
+  const void* v;
+  int64_t qs[4], ks[4], vs[4];
+  uint64_t* bits;         // [b][L][W]
+  int32_t* idx;           // [L][b][H][B] (or [b][H][B] for one layer)
+  void* k_out;            // [L][b][H][B][d]
+  void* v_out;
+};
+
+hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Workspace& w,
+                     hipStream_t s, hipEvent_t* ev);
+hipError_t run_score(const Geometry& g, const void* q, const int64_t qs[3], const void* k,
+                     const int64_t ks[3], float* p_raw, float* p_ext, float* imp, char* ws,
+                     const Workspace& w, hipStream_t s);
+hipError_t run_select(const Geometry& g, int layer, const float* p_raw, const float* p_ext,
+                      const float* imp, uint64_t* bits, int32_t* idx, uint32_t* htop, char* ws,
+                      const Workspace& w, hipStream_t s);
+hipError_t run_evict_layer(const Geometry& g, int layer, const ModelIO& m, char* ws,
+                           const Workspace& w, hipStream_t s);
+hipError_t run_compact(const Geometry& g, int n_layers, const ModelIO& m, hipStream_t s);
+hipError_t run_keep_all(const Geometry& g, int layer, uint64_t* bits, int32_t* idx, hipStream_t s);
+hipError_t run_coverage(const Geometry& g, const uint64_t* bits, int upto, int64_t* count,
+                        hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Device helpers
@@ -83,14 +94,8 @@ hipError_t launch_zero_bits(const Geometry& g, uint64_t* bits, hipStream_t s);
 
 // Order-preserving map of an IEEE float to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t float_key(float f) {
-  uint32_t u = __float_as_uint(f);
+  const uint32_t u = __float_as_uint(f);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
 }
 
 __device__ __forceinline__ double wave_sum(double v) {
@@ -110,8 +115,8 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Exclusive prefix sum over the whole work-group (blockDim.x a multiple of 64,
-// at most 1024).  `tmp` is >= 17 ints of shared memory.  Returns the
+// Exclusive prefix sum over the work-group (blockDim.x a multiple of 64, at
+// most 1024).  `tmp` holds >= 17 ints of shared memory.  Returns the
 // exclusive prefix; `total` receives the block sum.  Contains barriers.
 __device__ __forceinline__ int block_excl_scan(int v, int* tmp, int& total) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;

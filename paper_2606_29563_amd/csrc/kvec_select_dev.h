@@ -1,0 +1,493 @@
+// Selection stages of K-VEC (paper Algorithm 1, then the top-B of Sec. 4.1).
+//
+//   pool      max-pool of P and of the extended-window P along t, the
+//             float64 sums of pooled P and its square per block (sigma), and
+//             4096-bin histograms of both pooled scores per head.
+//   prep      per (sequence, head, token block): sigma of every head and
+//             H_top = the delta heads with the lowest sigma (Sec. 4.1); the
+//             head's selected score P_sel; then, from the histogram, a
+//             coverage-independent superset ("members") of every token that
+//             can be preserved or finally kept, in ascending token order.
+//   select    per (layer, sequence, head), run in layer order: the preserve
+//             set = first K tokens by (P_sel desc, t asc) (Sec. 4.2),
+//             P' = P_sel + lambda * I * (1 - n_t/(l+1)) in fp32 with one
+//             rounding per operation and P' = 1 on the preserve set, the first
+//             B-O by (P' desc, t asc) emitted in ascending order then the
+//             window, and the kept tokens OR-ed into the layer's bitmap row.
+//   count     the running coverage counts n_t of the pipeline.
+//
+// Why the superset is exact: for a non-preserved token, 0 <= bonus <=
+// lambda*I, so P_sel <= P' <= U = fl(P_sel + fl(lambda*I)) (fp32 rounding is
+// monotone).  The M = B-O tokens with the largest P_sel all have
+// P' >= min(P_sel, 1), so the M-th largest P' is >= min(c, 1) where c is the
+// M-th largest P_sel; a token with U < min(c, 1) can never be kept.  Every
+// token that can be preserved has P_sel >= the K-th largest P_sel.  Both
+// thresholds are replaced by the lower edge of the histogram bin holding
+// that order statistic, which only enlarges the superset.
+#pragma once
+
+#include "kvec_internal.h"
+
+namespace kvec {
+
+__device__ __forceinline__ float key_float(uint32_t k) {
+  const uint32_t u = (k & 0x80000000u) ? (k & 0x7fffffffu) : ~k;
+  return __uint_as_float(u);
+}
+
+// Pointers of one layer for the selection stages.
+struct SelectIO {
+  const float* psum_base;  // pipeline: score partials [b][n_rt][H][Tc]
+  const float* psum_all;
+  const float* ipart;      // [b][n_rt][Tc]
+  const float* p_raw;      // standalone: raw scores [b][H][Tc] (used when psum_* null)
+  const float* p_ext;
+  const float* imp_in;     // standalone: [b][Tc]
+  float* imp;              // [b][Tc] importance (written by pool in the pipeline)
+  float* pooled;           // [b][H][Tc]
+  float* pooled_ext;
+  double2* stats;          // [b][H][n_pool]
+  uint32_t* hist;          // [b][2][H][kHistBins]
+  int32_t* mem_t;          // [b][H][Tc] members of each prep chunk at chunk offsets
+  float* mem_ps;
+  float* mem_i;
+  int32_t* mem_n;          // [b][H][n_prep]
+  uint32_t* htop_mask;     // nullable [b]
+  uint32_t* spill_keys;    // [b][H][Tc] member arrays when members exceed the LDS capacity
+  int32_t* spill_t;
+  float* spill_ps;
+  float* spill_i;
+  const uint8_t* cnt_in;   // [b][T] counts of earlier layers (null: none)
+  const uint64_t* bits_prev; // bitmap row of the previous layer, [b] stride L*W (null: none)
+  uint64_t* bits;          // [b][L][W] coverage bitmap
+  int32_t* idx;            // [b][H][B] of this layer
+};
+
+// ---------------------------------------------------------------------------
+// pool: grid item (b, h, chunk); 512 threads
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, int b, int h,
+                                          int chunk, char* smem) {
+  const int r = P.pool / 2;
+  const int t0 = chunk * kPoolChunk;
+  const int t1 = min(P.Tc, t0 + kPoolChunk);
+  const int a0 = max(0, t0 - r), a1 = min(P.Tc, t1 + r);
+  float* sp = reinterpret_cast<float*>(smem);        // raw P   [a0, a1)
+  float* se = sp + (kPoolChunk + 64);                 // raw P'  [a0, a1)
+  uint32_t* hp = reinterpret_cast<uint32_t*>(se + (kPoolChunk + 64));
+  uint32_t* he = hp + kHistBins;
+  double* red = reinterpret_cast<double*>(he + kHistBins);
+  for (int i = threadIdx.x; i < 2 * kHistBins; i += blockDim.x) hp[i] = 0u;
+  const int64_t row = ((int64_t)b * P.H + h) * P.Tc;
+  for (int t = a0 + threadIdx.x; t < a1; t += blockDim.x) {
+    float vp, ve;
+    if (io.psum_all) {
+      float sb = 0.f, sa = 0.f;
+      for (int rt = 0; rt < P.n_rt; ++rt) {
+        const int64_t o = (((int64_t)b * P.n_rt + rt) * P.H + h) * P.Tc + t;
+        if (rt < P.n_rt_base) sb += io.psum_base[o];
+        sa += io.psum_all[o];
+      }
+      vp = sb * P.inv_go;
+      ve = sa * P.inv_gwn;
+    } else {
+      vp = io.p_raw[row + t];
+      ve = io.p_ext[row + t];
+    }
+    sp[t - a0] = vp;
+    se[t - a0] = ve;
+  }
+  if (h == 0 && io.psum_all) {
+    for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
+      float s = 0.f;
+      for (int rt = 0; rt < P.n_rt_base; ++rt) s += io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t];
+      io.imp[(int64_t)b * P.Tc + t] = s * P.inv_go;
+    }
+  }
+  __syncthreads();
+  double s1 = 0.0, s2 = 0.0;
+  for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
+    const int u0 = max(0, t - r), u1 = min(P.Tc - 1, t + r);
+    float m = sp[u0 - a0], me = se[u0 - a0];
+    for (int u = u0 + 1; u <= u1; ++u) {
+      m = fmaxf(m, sp[u - a0]);
+      me = fmaxf(me, se[u - a0]);
+    }
+    io.pooled[row + t] = m;
+    io.pooled_ext[row + t] = me;
+    s1 += (double)m;
+    s2 += (double)m * (double)m;
+    atomicAdd(&hp[float_key(m) >> (32 - kHistBits)], 1u);
+    atomicAdd(&he[float_key(me) >> (32 - kHistBits)], 1u);
+  }
+  s1 = wave_sum(s1);
+  s2 = wave_sum(s2);
+  const int wid = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[2 * wid] = s1;
+    red[2 * wid + 1] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double a1 = 0.0, a2 = 0.0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
+      a1 += red[2 * i];
+      a2 += red[2 * i + 1];
+    }
+    io.stats[((int64_t)b * P.H + h) * P.n_pool + chunk] = make_double2(a1, a2);
+  }
+  uint32_t* gh = io.hist + ((int64_t)b * 2 * P.H) * kHistBins;
+  for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
+    if (hp[i]) atomicAdd(&gh[(int64_t)h * kHistBins + i], hp[i]);
+    if (he[i]) atomicAdd(&gh[(int64_t)(P.H + h) * kHistBins + i], he[i]);
+  }
+}
+
+// Bin holding the k-th largest key (1 <= k <= total) of a histogram, by a
+// block-wide descending prefix sum.  Returns -1 for k <= 0.
+__device__ __forceinline__ int hist_bin_of_rank(const uint32_t* gh, int k, int* tmp) {
+  if (k <= 0) return -1;
+  constexpr int per = kHistBins / 512;
+  const int tid = threadIdx.x;  // owns bins [kHistBins-1-tid*per, ... descending)
+  int cnt[per], s = 0;
+#pragma unroll
+  for (int e = 0; e < per; ++e) {
+    cnt[e] = (int)gh[kHistBins - 1 - (tid * per + e)];
+    s += cnt[e];
+  }
+  int total;
+  const int before = block_excl_scan(s, tmp, total);
+  if (before < k && k <= before + s) {
+    int run = before, found = -1;
+#pragma unroll
+    for (int e = 0; e < per; ++e) {
+      if (found < 0 && run + cnt[e] >= k) found = e;
+      run += cnt[e];
+    }
+    tmp[20] = kHistBins - 1 - (tid * per + found);
+  }
+  __syncthreads();
+  const int bin = tmp[20];
+  __syncthreads();
+  return bin;
+}
+
+// ---------------------------------------------------------------------------
+// prep: grid item (b, h, chunk); 512 threads
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, int layer, int b,
+                                          int h, int chunk, char* smem) {
+  if (h == 0 && chunk == 0) {
+    // the selection of this layer ORs its kept tokens into a cleared row
+    uint64_t* row = io.bits + ((int64_t)b * P.L + layer) * P.words;
+    for (int i = threadIdx.x; i < P.words; i += blockDim.x) row[i] = 0ull;
+  }
+  double* var = reinterpret_cast<double*>(smem);
+  int* in_top = reinterpret_cast<int*>(var + 8);
+  int* tmp = in_top + 8;
+  if ((int)threadIdx.x < P.H) {
+    const int g = threadIdx.x;
+    double a1 = 0.0, a2 = 0.0;
+    for (int i = 0; i < P.n_pool; ++i) {
+      const double2 v = io.stats[((int64_t)b * P.H + g) * P.n_pool + i];
+      a1 += v.x;
+      a2 += v.y;
+    }
+    const double mean = a1 / P.Tc;
+    var[g] = a2 / P.Tc - mean * mean;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < P.H) {
+    const int g = threadIdx.x;
+    int rank = 0;
+    for (int o = 0; o < P.H; ++o) rank += (var[o] < var[g]) || (var[o] == var[g] && o < g);
+    in_top[g] = rank < P.delta_eff;
+  }
+  __syncthreads();
+  if (h == 0 && chunk == 0 && threadIdx.x == 0 && io.htop_mask) {
+    uint32_t m = 0;
+    for (int g = 0; g < P.H; ++g) m |= (uint32_t)in_top[g] << g;
+    io.htop_mask[b] = m;
+  }
+  const bool ext = in_top[h] != 0;
+  const float* src = (ext ? io.pooled_ext : io.pooled) + ((int64_t)b * P.H + h) * P.Tc;
+  const uint32_t* gh = io.hist + ((int64_t)b * 2 * P.H + (ext ? P.H : 0) + h) * kHistBins;
+  const int bin_kp = hist_bin_of_rank(gh, P.Kp, tmp);
+  const int bin_m = hist_bin_of_rank(gh, P.M, tmp);
+  const uint32_t kp_edge = bin_kp < 0 ? 0xffffffffu : (uint32_t)bin_kp << (32 - kHistBits);
+  const float c_edge = bin_m < 0 ? INFINITY : key_float((uint32_t)bin_m << (32 - kHistBits));
+  const float thr_u = fminf(c_edge, 1.0f);
+  const bool has_preserve = bin_kp >= 0;
+  // Members of this chunk in ascending order: blocked layout, 8 tokens per thread.
+  const int t0 = chunk * kPrepChunk;
+  const int t1 = min(P.Tc, t0 + kPrepChunk);
+  constexpr int per = kPrepChunk / 512;
+  const int lo = min(t1, t0 + (int)threadIdx.x * per), hi = min(t1, lo + per);
+  const float* imp = io.imp + (int64_t)b * P.Tc;
+  unsigned flags = 0;
+  int cntm = 0;
+  for (int t = lo; t < hi; ++t) {
+    const float ps = src[t];
+    const float u = __fadd_rn(ps, __fmul_rn(P.lam, imp[t]));
+    const bool m = (has_preserve && float_key(ps) >= kp_edge) || u >= thr_u;
+    flags |= (unsigned)m << (t - lo);
+    cntm += m;
+  }
+  int total;
+  int o = block_excl_scan(cntm, tmp, total);
+  const int64_t base = ((int64_t)b * P.H + h) * P.Tc + t0;
+  for (int t = lo; t < hi; ++t) {
+    if ((flags >> (t - lo)) & 1u) {
+      io.mem_t[base + o] = t;
+      io.mem_ps[base + o] = src[t];
+      io.mem_i[base + o] = imp[t];
+      ++o;
+    }
+  }
+  if (threadIdx.x == 0) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = total;
+}
+
+// ---------------------------------------------------------------------------
+// select: one work-group per (layer, sequence, head)
+// ---------------------------------------------------------------------------
+
+// Block radix select over keys k[0..n) (512 threads): the first `want` keys in
+// the order (key desc, index asc) are those > thr plus the first `take` keys
+// equal to thr.  Three passes of 11, 11 and 10 bits over an LDS histogram.
+__device__ __forceinline__ void block_radix_select(const uint32_t* kb, int n, int want,
+                                                   uint32_t* hist, int* tmp, uint32_t& thr,
+                                                   int& take) {
+  uint32_t prefix = 0, mask = 0;
+  int rem = want;
+  const int shifts[3] = {21, 10, 0};
+  const int widths[3] = {11, 11, 10};
+#pragma unroll
+  for (int ps = 0; ps < 3; ++ps) {
+    const int shift = shifts[ps], nb = 1 << widths[ps];
+    const uint32_t dm = (uint32_t)nb - 1u;
+    for (int i = threadIdx.x; i < nb; i += blockDim.x) hist[i] = 0u;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+      const uint32_t kk = kb[i];
+      if ((kk & mask) == prefix) atomicAdd(&hist[(kk >> shift) & dm], 1u);
+    }
+    __syncthreads();
+    // descending order: thread owns bins nb-1-tid*per .. nb-per-tid*per
+    const int per = nb / (int)blockDim.x;
+    int cnt[4] = {0, 0, 0, 0}, sum = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (e < per) {
+        cnt[e] = (int)hist[nb - 1 - ((int)threadIdx.x * per + e)];
+        sum += cnt[e];
+      }
+    int total;
+    const int before = block_excl_scan(sum, tmp, total);
+    if (before < rem && rem <= before + sum) {
+      int run = before;
+      bool found = false;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if (e < per && !found && run + cnt[e] >= rem) {
+          tmp[20] = nb - 1 - ((int)threadIdx.x * per + e);
+          tmp[21] = rem - run;
+          found = true;
+        } else if (e < per) {
+          run += cnt[e];
+        }
+    }
+    __syncthreads();
+    prefix |= (uint32_t)tmp[20] << shift;
+    mask |= dm << shift;
+    rem = tmp[21];
+    __syncthreads();
+  }
+  thr = prefix;
+  take = rem;
+}
+
+// Flags of the first `want` members (given thr/take from the radix select),
+// in member order, by a blocked prefix count of the keys equal to thr.
+// Calls fn(i, selected) for every member i of this thread's block range.
+template <class Fn>
+__device__ __forceinline__ void block_flags(const uint32_t* kb, int n, int want, uint32_t thr,
+                                            int take, int* tmp, Fn fn) {
+  const int per = (n + blockDim.x - 1) / blockDim.x;
+  const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
+  int ceq = 0;
+  for (int i = lo; i < hi; ++i) ceq += kb[i] == thr;
+  int total;
+  int e = block_excl_scan(ceq, tmp, total);
+  for (int i = lo; i < hi; ++i) {
+    const uint32_t kk = kb[i];
+    bool sel;
+    if (want >= n) {
+      sel = true;
+    } else if (want <= 0) {
+      sel = false;
+    } else {
+      sel = kk > thr || (kk == thr && e < take);
+      e += kk == thr;
+    }
+    fn(i, sel);
+  }
+}
+
+__device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io, int layer, int b,
+                                            int h, char* smem) {
+  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);    // [2048]
+  int* tmp = reinterpret_cast<int*>(hist + 2048);          // [32]
+  int* off = tmp + 32;                                     // [n_prep + 1] member offsets
+  char* marr = reinterpret_cast<char*>(off + ((P.n_prep + 1 + 3) & ~3));
+  const int64_t hb = (int64_t)b * P.H + h;
+  const int32_t* mn = io.mem_n + hb * P.n_prep;
+  // member offsets of the prep chunks
+  if (threadIdx.x == 0) {
+    int acc = 0;
+    for (int c = 0; c < P.n_prep; ++c) {
+      off[c] = acc;
+      acc += mn[c];
+    }
+    off[P.n_prep] = acc;
+  }
+  __syncthreads();
+  const int n = off[P.n_prep];
+  uint32_t* kb;
+  int32_t* mt;
+  float *mp, *mi;
+  if (n <= P.mcap) {
+    kb = reinterpret_cast<uint32_t*>(marr);
+    mt = reinterpret_cast<int32_t*>(kb + P.mcap);
+    mp = reinterpret_cast<float*>(mt + P.mcap);
+    mi = mp + P.mcap;
+  } else {
+    kb = io.spill_keys + hb * P.Tc;
+    mt = io.spill_t + hb * P.Tc;
+    mp = io.spill_ps + hb * P.Tc;
+    mi = io.spill_i + hb * P.Tc;
+  }
+  // gather the members contiguously (ascending t), with their preserve keys
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    int lo = 0, hi = P.n_prep - 1;  // chunk c with off[c] <= i < off[c+1]
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (off[mid] <= i) lo = mid; else hi = mid - 1;
+    }
+    const int64_t g = hb * P.Tc + (int64_t)lo * kPrepChunk + (i - off[lo]);
+    const float ps = io.mem_ps[g];
+    mt[i] = io.mem_t[g];
+    mp[i] = ps;
+    mi[i] = io.mem_i[g];
+    kb[i] = float_key(ps);
+  }
+  __syncthreads();
+  // 1. preserve set: first Kp members by (P_sel desc, t asc)
+  const int kp = min(P.Kp, n);
+  uint32_t thr_p = 0xffffffffu;
+  int take_p = 0;
+  if (kp > 0 && kp < n) block_radix_select(kb, n, kp, hist, tmp, thr_p, take_p);
+  // 2. P' keys: 1.0 on the preserve set, else P_sel + lambda * I * (1 - n_t/(l+1))
+  const float f_denom = (float)(layer + 1);
+  const uint8_t* cnt = io.cnt_in;
+  const uint64_t* prow = io.bits_prev;
+  block_flags(kb, n, kp, thr_p, take_p, tmp, [&](int i, bool pres) {
+    float pp;
+    if (pres) {
+      pp = 1.0f;
+    } else {
+      const int t = mt[i];
+      int nt = cnt ? (int)cnt[(int64_t)b * P.T + t] : 0;
+      if (prow) nt += (int)((prow[(int64_t)b * P.L * P.words + (t >> 6)] >> (t & 63)) & 1ull);
+      const float cov = __fdiv_rn((float)nt, f_denom);
+      const float focus = __fmul_rn(mi[i], __fsub_rn(1.0f, cov));
+      pp = __fadd_rn(mp[i], __fmul_rn(P.lam, focus));
+    }
+    kb[i] = float_key(pp);
+  });
+  __syncthreads();
+  // 3. final pick: first M members by (P' desc, t asc), emitted in ascending order
+  const int m = min(P.M, n);
+  uint32_t thr = 0xffffffffu;
+  int take = 0;
+  if (m > 0 && m < n) block_radix_select(kb, n, m, hist, tmp, thr, take);
+  // output positions: blocked count of the selected members, then emission
+  const int per = (n + blockDim.x - 1) / blockDim.x;
+  const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
+  int ceq = 0;
+  for (int i = lo; i < hi; ++i) ceq += kb[i] == thr;
+  int total;
+  const int e0 = block_excl_scan(ceq, tmp, total);
+  auto selected = [&](uint32_t kk, int& e) {
+    if (m >= n) return true;
+    if (m <= 0) return false;
+    const bool eq = kk == thr;
+    const bool sel = kk > thr || (eq && e < take);
+    e += eq;
+    return sel;
+  };
+  int csel = 0;
+  {
+    int e = e0;
+    for (int i = lo; i < hi; ++i) csel += selected(kb[i], e);
+  }
+  int o = block_excl_scan(csel, tmp, total);
+  int32_t* out = io.idx + hb * P.B;
+  uint64_t* row = io.bits + ((int64_t)b * P.L + layer) * P.words;
+  uint64_t word = 0;
+  int cur = -1;
+  {
+    int e = e0;
+    for (int i = lo; i < hi; ++i) {
+      if (!selected(kb[i], e)) continue;
+      const int t = mt[i];
+      out[o++] = t;
+      if ((t >> 6) != cur) {
+        if (cur >= 0) atomicOr((unsigned long long*)&row[cur], (unsigned long long)word);
+        cur = t >> 6;
+        word = 0;
+      }
+      word |= 1ull << (t & 63);
+    }
+  }
+  if (cur >= 0) atomicOr((unsigned long long*)&row[cur], (unsigned long long)word);
+  for (int i = threadIdx.x; i < P.O; i += blockDim.x) out[P.M + i] = P.Tc + i;
+  if (h == 0) {
+    // the observation window is always kept
+    for (int t = P.Tc + threadIdx.x; t < P.T; t += blockDim.x)
+      atomicOr((unsigned long long*)&row[t >> 6], 1ull << (t & 63));
+  }
+}
+
+// Running coverage counts of the pipeline: n_t(layer) = n_t(layer-1) + kept
+// bit of layer-1, into the buffer of this layer's parity (the next layer's
+// selection adds this layer's bitmap row itself).  Part `part` of kCountWords
+// bitmap words.
+constexpr int kCountWords = 64;
+
+__device__ __forceinline__ void task_count(const Problem& P, const uint8_t* cnt_prev,
+                                           const uint64_t* row_prev, uint8_t* cnt_out, int b,
+                                           int part) {
+  const int w0 = part * kCountWords;
+  for (int i = threadIdx.x; i < kCountWords * 64; i += blockDim.x) {
+    const int wi = w0 + i / 64, t = wi * 64 + (i & 63);
+    if (wi >= P.words || t >= P.T) continue;
+    int v = 0;
+    if (cnt_prev) v = (int)cnt_prev[(int64_t)b * P.T + t];
+    if (row_prev) v += (int)((row_prev[(int64_t)b * P.L * P.words + wi] >> (t & 63)) & 1ull);
+    cnt_out[(int64_t)b * P.T + t] = (uint8_t)v;
+  }
+}
+
+// n_t for a standalone layer call: counts of the caller's bitmap rows < layer.
+__device__ __forceinline__ void task_counts_from_bits(const Problem& P, const uint64_t* bits,
+                                                      uint8_t* counts, int layer, int b, int wi) {
+  const int tlo = wi * 64;
+  for (int t = tlo + (int)threadIdx.x; t < min(tlo + 64, P.T); t += blockDim.x) {
+    int nt = 0;
+    for (int l = 0; l < layer; ++l)
+      nt += (int)((bits[((int64_t)b * P.L + l) * P.words + wi] >> (t - tlo)) & 1ull);
+    counts[(int64_t)b * P.T + t] = (uint8_t)nt;
+  }
+}
+
+}  // namespace kvec

@@ -82,7 +82,8 @@ class Config:
 _lib = None
 
 EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_select_cover", "kvec_compact",
-           "kvec_evict_layer", "kvec_evict_model", "kvec_coverage", "kvec_status_string"]
+           "kvec_evict_layer", "kvec_evict_model", "kvec_profile_points", "kvec_coverage",
+           "kvec_status_string"]
 
 
 def load() -> ctypes.CDLL:
@@ -105,11 +106,13 @@ def load() -> ctypes.CDLL:
     lib.kvec_evict_model.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp, sz, vp,
                                      ctypes.POINTER(vp)]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
+    lib.kvec_profile_points.argtypes = [P]
     lib.kvec_status_string.argtypes = [ctypes.c_int]
     lib.kvec_status_string.restype = ctypes.c_char_p
     for name in EXPORTS:
-        if name != "kvec_status_string":
+        if name not in ("kvec_status_string", "kvec_profile_points"):
             getattr(lib, name).restype = ctypes.c_int
+    lib.kvec_profile_points.restype = ctypes.c_int32
     _lib = lib
     return lib
 
@@ -185,7 +188,7 @@ def kvec_evict_layer(cfg: Config, layer: int, q_win, k, v, cover_bits, idx, k_ou
 def kvec_evict_model(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, ws, stream=None,
                      events=None) -> None:
     """q_win [L][b][HQ][O'][d], k/v [L][b][H][T][d]; idx [L][b][H][B]; k_out/v_out [L][b][H][B][d].
-    events: optional sequence of 4*L raw hipEvent_t handles (ints)."""
+    events: optional sequence of kvec_profile_points(cfg) raw hipEvent_t handles (ints)."""
     c = cfg.c()
     ev = None
     if events is not None:
@@ -195,6 +198,11 @@ def kvec_evict_model(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, ws
                                    _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream), ev),
            "kvec_evict_model")
+
+
+def kvec_profile_points(cfg: Config) -> int:
+    c = cfg.c()
+    return int(load().kvec_profile_points(ctypes.byref(c)))
 
 
 def kvec_coverage(cfg: Config, cover_bits, upto_layer: int, count, stream=None) -> None:

@@ -14,7 +14,7 @@ HEADER = os.path.join(ROOT, "include", "kvec.h")
 
 def _declared():
     src = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:kvec_status|const char\*)\s+(kvec_\w+)\s*\(", src, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:kvec_status|const char\*|int32_t)\s+(kvec_\w+)\s*\(", src, re.M)))
 
 
 def test_header_declares_expected_calls():
@@ -73,7 +73,10 @@ def test_workspace_size_positive_and_monotone():
     (dict(dtype=7), kvec.KVEC_ERR_INVALID),
     (dict(head_dim=96), kvec.KVEC_ERR_UNSUPPORTED),
     (dict(n_q_heads=24), kvec.KVEC_ERR_UNSUPPORTED),        # G = 3
-    (dict(n_kv_heads=32, n_q_heads=32), kvec.KVEC_ERR_UNSUPPORTED),
+    (dict(n_kv_heads=16, n_q_heads=32), kvec.KVEC_ERR_UNSUPPORTED),
+    (dict(n_kv_heads=3, n_q_heads=12), kvec.KVEC_ERR_UNSUPPORTED),
+    (dict(seq_len=300000), kvec.KVEC_ERR_UNSUPPORTED),
+    (dict(pool_kernel=65), kvec.KVEC_ERR_UNSUPPORTED),
 ])
 def test_config_validation(over, code):
     st, _ = _ws_status(_cfg(**over))

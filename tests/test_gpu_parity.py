@@ -34,7 +34,8 @@ SCORE_CASES = [
     _small("f32-d64-g2-ragged", 301, 32, 64, 4, 2, 64, "f32", rope=False),
     _small("bf16-d128-g4", 1000, 32, 64, 8, 4, 128, "bf16"),
     _small("bf16-d128-g4-mixed", 777, 20, 40, 2, 4, 128, "bf16"),
-    _small("bf16-d64-g1-pad", 530, 20, 40, 3, 1, 64, "bf16"),
+    _small("bf16-d64-g1-pad", 530, 20, 40, 2, 1, 64, "bf16"),
+    _small("bf16-d128-g2-h1", 3001, 24, 48, 1, 2, 128, "bf16"),
     _small("bf16-d128-g4-o64", 2048, 64, 128, 8, 4, 128, "bf16", batch=2),
     _small("bf16-d128-g8", 257, 5, 17, 2, 8, 128, "bf16"),
     _small("bf16-d64-g2-short", 70, 16, 64, 2, 2, 64, "bf16"),
@@ -80,7 +81,8 @@ SELECT_CASES = [
     _small("sel-beta0", 1500, 16, 32, 4, 2, 64, "bf16", B=100, layers=3, beta=0.0),
     _small("sel-beta1", 1500, 16, 32, 4, 2, 64, "bf16", B=100, layers=3, beta=1.0),
     _small("sel-wn-eq-o", 1500, 16, 16, 4, 2, 64, "bf16", B=100, layers=3),
-    _small("sel-ragged", 999, 7, 14, 3, 1, 64, "bf16", B=41, layers=3, pool=3),
+    _small("sel-ragged", 999, 7, 14, 2, 1, 64, "bf16", B=41, layers=3, pool=3),
+    _small("sel-long", 20000, 32, 64, 8, 4, 128, "bf16", B=700, layers=3),
 ]
 
 
@@ -145,13 +147,13 @@ def test_keep_everything_when_budget_covers(gpu_lib):
 def test_compact_bit_exact(gpu_lib):
     import torch
     kv = gpu_lib
-    w = _small("compact", 500, 8, 16, 3, 2, 128, "bf16", batch=2, B=64, layers=1)
+    w = _small("compact", 500, 8, 16, 4, 2, 128, "bf16", batch=2, B=64, layers=1)
     cfg = kv.Config.from_workload(w)
     g = torch.Generator().manual_seed(3)
-    k = torch.randn((2, 3, 500, 128), generator=g).to(torch.bfloat16).cuda()
-    v = torch.randn((2, 3, 500, 128), generator=g).to(torch.bfloat16).cuda()
-    idx = torch.randint(-1, 500, (2, 3, 64), generator=g, dtype=torch.int32).cuda()
-    ko = torch.empty((2, 3, 64, 128), dtype=torch.bfloat16, device="cuda")
+    k = torch.randn((2, 4, 500, 128), generator=g).to(torch.bfloat16).cuda()
+    v = torch.randn((2, 4, 500, 128), generator=g).to(torch.bfloat16).cuda()
+    idx = torch.randint(-1, 500, (2, 4, 64), generator=g, dtype=torch.int32).cuda()
+    ko = torch.empty((2, 4, 64, 128), dtype=torch.bfloat16, device="cuda")
     vo = torch.empty_like(ko)
     kv.kvec_compact(cfg, k, v, idx, ko, vo)
     torch.cuda.synchronize()
@@ -224,3 +226,31 @@ def test_e2e_tiny_fp32(gpu_lib):
 
 def test_e2e_small_bf16(gpu_lib):
     _e2e(gpu_lib, _small("e2e-small", 2500, 32, 64, 8, 4, 128, "bf16", B=200, layers=6))
+
+
+def test_layer_calls_match_model_step(gpu_lib):
+    """kvec_evict_layer called layer by layer reproduces kvec_evict_model exactly."""
+    import torch
+    kv = gpu_lib
+    w = _small("layerwise", 3000, 32, 64, 4, 4, 128, "bf16", batch=2, B=256, layers=5)
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    q, k, v = model_tensors(w)
+    L, H, B, T, d = w.n_layers, w.n_kv_heads, w.budget, w.seq_len, w.head_dim
+    W = (T + 63) // 64
+    bits_m = torch.empty((w.batch, L, W), dtype=torch.int64, device="cuda")
+    idx_m = torch.empty((L, w.batch, H, B), dtype=torch.int32, device="cuda")
+    ko_m = torch.empty((L, w.batch, H, B, d), dtype=k.dtype, device="cuda")
+    vo_m = torch.empty_like(ko_m)
+    kv.kvec_evict_model(cfg, q, k, v, bits_m, idx_m, ko_m, vo_m, ws)
+    bits_l = torch.zeros_like(bits_m)
+    idx_l = torch.empty_like(idx_m)
+    ko_l = torch.empty_like(ko_m)
+    vo_l = torch.empty_like(vo_m)
+    for l in range(L):
+        kv.kvec_evict_layer(cfg, l, q[l], k[l], v[l], bits_l, idx_l[l], ko_l[l], vo_l[l], ws)
+    torch.cuda.synchronize()
+    assert torch.equal(idx_m, idx_l)
+    assert torch.equal(bits_m, bits_l)
+    assert torch.equal(ko_m.view(torch.int16), ko_l.view(torch.int16))
+    assert torch.equal(vo_m.view(torch.int16), vo_l.view(torch.int16))
