@@ -64,10 +64,15 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   x.n_rtg = (x.n_rt + tpw - 1) / tpw;
   x.n_kt1 = (x.T + kTile1 - 1) / kTile1;
   x.n_kt2 = (x.Tc + kTile2 - 1) / kTile2;
+  // pass-2 LDS: the key ring plus, per row tile, the importance exchange
+  // (H * WR * SK), its reduction, the staged per-key sums and importance
+  const size_t ring = key_ring_bytes(c->dtype == KVEC_BF16 ? 2 : 4, x.D);
+  auto lds_p2 = [&](int sk) {
+    return ring + (size_t)tpw * ((size_t)H * x.WR * sk + 64 * H + 2 * H * kTile2 + kTile2) * 4;
+  };
   x.SK = 64;
-  while (x.SK > 16 && ((size_t)tpw * ((size_t)H * x.WR * x.SK + 64 * H + 2 * H * kTile2 + kTile2)) * 4 >
-                          98304)
-    x.SK /= 2;
+  while (x.SK > 16 && lds_p2(x.SK) > kLdsMax - kLdsStatic) x.SK /= 2;
+  if (lds_p2(x.SK) > kLdsMax - kLdsStatic) return KVEC_ERR_UNSUPPORTED;
   x.n_pool = (x.Tc + kPoolChunk - 1) / kPoolChunk;
   x.n_prep = (x.Tc + kPrepChunk - 1) / kPrepChunk;
   x.words = (x.T + 63) / 64;
@@ -118,6 +123,7 @@ Workspace make_workspace(const Geometry& g) {
   // dynamic LDS: the largest task
   const int tpw = 8 / P.H;
   const size_t lds_p2 =
+      key_ring_bytes(P.esize, P.D) +
       (size_t)tpw * ((size_t)P.H * P.WR * P.SK + 64 * P.H + 2 * P.H * kTile2 + kTile2) * 4;
   const size_t lds_pool = (size_t)(2 * (kPoolChunk + 64) + 2 * kHistBins) * 4 + 16 * 8;
   const size_t lds_prep = 256;
@@ -144,6 +150,12 @@ bool strides_ok(const int64_t* s, int n, int esize) {
   for (int i = 0; i < n; ++i)
     if (s[i] < 0 || (s[i] * esize) % 16 != 0) return false;
   return true;
+}
+
+// The score passes address the keys of one (batch, head) with 32-bit buffer
+// offsets: T rows of k_strides[t] elements must span less than 2 GiB.
+bool keys_addressable(const Problem& P, int64_t t_stride) {
+  return (int64_t)P.T * t_stride * P.esize < ((int64_t)1 << 31);
 }
 
 kvec_status dev(hipError_t e) { return e == hipSuccess ? KVEC_OK : KVEC_ERR_DEVICE; }
@@ -185,6 +197,7 @@ kvec_status kvec_score(const kvec_config* cfg, const void* q_win, const int64_t 
   if (!aligned16(q_win) || !aligned16(k) || !strides_ok(q_strides, 3, g.p.esize) ||
       !strides_ok(k_strides, 3, g.p.esize) || !p_raw || !p_ext_raw || !imp)
     return KVEC_ERR_INVALID;
+  if (!keys_addressable(g.p, k_strides[2])) return KVEC_ERR_UNSUPPORTED;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
   return dev(run_score(g, q_win, q_strides, k, k_strides, p_raw, p_ext_raw, imp,
@@ -242,6 +255,7 @@ kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* 
     return KVEC_ERR_INVALID;
   if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 3, g.p.esize)))
     return KVEC_ERR_INVALID;
+  if (!g.keep_all && !keys_addressable(g.p, k_strides[2])) return KVEC_ERR_UNSUPPORTED;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
   ModelIO m;
@@ -278,6 +292,7 @@ kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const in
     return KVEC_ERR_INVALID;
   if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 4, g.p.esize)))
     return KVEC_ERR_INVALID;
+  if (!g.keep_all && !keys_addressable(g.p, k_strides[3])) return KVEC_ERR_UNSUPPORTED;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
   ModelIO m;

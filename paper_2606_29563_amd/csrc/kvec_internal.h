@@ -31,6 +31,16 @@ struct Tiling {
 
 inline int row_blocks_per_tile(int G) { return G >= 4 ? 1 : 4 / G; }
 
+// Key staging of the score passes: each wave streams its keys, 16 per step,
+// through a private ring of LDS slots (16 * D * esize bytes each).  Deeper
+// rings for small slots; fp32 with d = 128 keeps a single slot.
+constexpr int key_ring_slots(int esize, int D) {
+  return 16 * D * esize <= 2048 ? 4 : 16 * D * esize <= 4096 ? 3 : 1;
+}
+constexpr size_t key_ring_bytes(int esize, int D) {
+  return (size_t)(kThreads / 64) * key_ring_slots(esize, D) * 16 * D * esize;
+}
+
 // Problem geometry visible to device code.
 struct Problem {
   int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;

@@ -18,11 +18,20 @@
 //
 // MFMA mapping (v_mfma_f32_16x16x32_bf16, or 16x16x4_f32 for fp32 inputs):
 // A = 16 query rows x 32 head-dim elements, B = 32 elements x 16 keys.  Lane
-// l supplies row/key (l % 16) and the head-dim slice [c*D/4, (c+1)*D/4) with
-// c = l / 16, split into k-steps; the dot product is order-free, so this
-// permutation of the reduction index is legal and gives each lane one
-// contiguous D/4-element load per row or key.  The output lane l holds rows
-// 4c..4c+3 of the block for key (l % 16).  A wave owns one KV head and
+// l supplies row/key (l % 16); with c = l / 16, its 16-byte piece c of each
+// 64-byte span of the row feeds one k-step (for fp32 the four floats of a
+// piece go to four k-steps, a permutation of the reduction index, which the
+// dot product allows).  The output lane l holds rows 4c..4c+3 of the block
+// for key (l % 16).
+//
+// Keys reach the MFMA through LDS: in that layout the lanes of one load
+// would touch 16 different rows, which the vector memory pipeline serves one
+// lane at a time.  Instead each wave copies its next 16 keys with direct
+// global-to-LDS loads in which consecutive lanes read consecutive 16-byte
+// pieces (whole rows, fully coalesced), into a private ring of LDS slots,
+// and reads its fragments back with ds_read_b128.  Piece q of key n is
+// stored at position q ^ (n mod 16), so the 16 keys a fragment read touches
+// fall in distinct LDS banks.  A wave owns one KV head and
 // NB = G*RB blocks: rows ordered (g, window row), so the G query heads of one
 // window row land in the same lane and their mean is a register sum.
 // Work-groups are 8 waves: 8/H row tiles of H heads each.
@@ -48,13 +57,19 @@ struct Frag<BF16, D> {
   static constexpr int KS = D / 32;
   bf16x8 v[KS];
   __device__ __forceinline__ void load(const void* row, int c) {
-    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(row) + c * (D / 4));
+    const uint4* p = static_cast<const uint4*>(row);
 #pragma unroll
-    for (int j = 0; j < KS; ++j) v[j] = __builtin_bit_cast(bf16x8, p[j]);
+    for (int j = 0; j < KS; ++j) v[j] = __builtin_bit_cast(bf16x8, p[4 * j + c]);
   }
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int j = 0; j < KS; ++j) v[j] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+  }
+  // key n of a swizzled LDS slot (rows of D*2 bytes, 16-byte pieces)
+  __device__ __forceinline__ void load_lds(const uint4* slot, int n, int c, int swz) {
+    const uint4* row = slot + n * (D / 8);
+#pragma unroll
+    for (int j = 0; j < KS; ++j) v[j] = __builtin_bit_cast(bf16x8, row[(4 * j + c) ^ (n & swz)]);
   }
 };
 
@@ -63,10 +78,10 @@ struct Frag<F32, D> {
   static constexpr int KS = D / 4;
   float v[KS];
   __device__ __forceinline__ void load(const void* row, int c) {
-    const uint4* p = reinterpret_cast<const uint4*>(static_cast<const float*>(row) + c * (D / 4));
+    const uint4* p = static_cast<const uint4*>(row);
 #pragma unroll
     for (int j = 0; j < KS / 4; ++j) {
-      const uint4 u = p[j];
+      const uint4 u = p[4 * j + c];
       v[4 * j + 0] = __uint_as_float(u.x);
       v[4 * j + 1] = __uint_as_float(u.y);
       v[4 * j + 2] = __uint_as_float(u.z);
@@ -76,6 +91,18 @@ struct Frag<F32, D> {
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int j = 0; j < KS; ++j) v[j] = 0.f;
+  }
+  // key n of a swizzled LDS slot (rows of D*4 bytes, 16-byte pieces)
+  __device__ __forceinline__ void load_lds(const uint4* slot, int n, int c, int swz) {
+    const uint4* row = slot + n * (D / 4);
+#pragma unroll
+    for (int j = 0; j < KS / 4; ++j) {
+      const uint4 u = row[(4 * j + c) ^ (n & swz)];
+      v[4 * j + 0] = __uint_as_float(u.x);
+      v[4 * j + 1] = __uint_as_float(u.y);
+      v[4 * j + 2] = __uint_as_float(u.z);
+      v[4 * j + 3] = __uint_as_float(u.w);
+    }
   }
 };
 
@@ -98,12 +125,22 @@ __device__ __forceinline__ f32x4 mma(const Frag<F32, D>& a, const Frag<F32, D>& 
 template <class TT>
 constexpr int elem_bytes() { return __is_same(TT, BF16) ? 2 : 4; }
 
-// Work-group barrier that orders LDS only: pending global loads (the K
-// prefetch ring) stay in flight across it.
+// Wait until at most N vector memory operations of this wave are pending.
+// Direct global-to-LDS loads are not tracked by the compiler's own waits, so
+// the key ring waits explicitly; the asm statement also keeps LDS reads from
+// being scheduled above it.
+template <int N>
+__device__ __forceinline__ void wait_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Work-group barrier that orders LDS only: this wave's LDS operations have
+// completed (lgkmcnt) before it arrives.  Written out because the compiler's
+// release fence would also drain the key ring's direct-to-LDS loads, which
+// must stay in flight across the barrier.
 __device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Combine two (max, sum of 2^(x - max)) pairs.
@@ -131,19 +168,34 @@ struct ScoreIO {
   float* ipart;       // [b][n_rt][Tc]
 };
 
-constexpr int kPrefetch = 4;  // K fragments in flight per wave (divides the steps of a tile)
+// Word 3 of a raw buffer resource on the gfx9 family (32-bit data format,
+// no swizzle); loads outside num_records return zero.
+constexpr int kBufferWord3 = 0x00020000;
+
+// Per-wave LDS ring of key steps (16 keys per step).
+template <class TT, int D>
+struct KeyRing {
+  static constexpr int ES = elem_bytes<TT>();
+  static constexpr int CPR = D * ES / 16;                // 16-byte pieces per key row
+  static constexpr int SWZ = (CPR < 16 ? CPR : 16) - 1;  // piece swizzle mask
+  static constexpr int SLOT = 16 * CPR * 16;             // bytes per step
+  static constexpr int NI = CPR / 4;                     // 1 KiB loads per step
+  static constexpr int KPI = 64 / CPR;                   // keys per load
+  static constexpr int R = key_ring_slots(ES, D);        // slots (steps in flight)
+  static_assert((size_t)(kThreads / 64) * R * SLOT == key_ring_bytes(ES, D), "ring size");
+};
 
 // One pass over one key tile for the row tiles of this work-group.
 // Block: 512 threads; wave w -> head w % H, row tile rtg*(8/H) + w / H.
 // The state lives in a struct whose methods are all force-inlined, so every
 // array is indexed by compile-time constants and stays in registers.
-#ifndef KVEC_PIPELINE_MMA
-#define KVEC_PIPELINE_MMA 1
-#endif
-// When set, the matrix products of step s+1 are issued before the exponentials
-// of step s (two accumulator sets); otherwise each step multiplies, then
-// exponentiates.
-constexpr bool kPipelineMma = KVEC_PIPELINE_MMA != 0;
+//
+// Pass 1 accumulates sum 2^(x - M) per row, with one reference M per 16-row
+// block, uniform across the wave: the largest logit of the block's rows at
+// the tile's first 16 keys.  A row whose logits later exceed M by more than
+// the fp32 exponent range (sum overflows) or stay far below it (sum < 2^-64,
+// so low bits could be lost) is flagged with an infinite sum and the row
+// normaliser recomputes that (row, tile) partial exactly.
 
 template <class TT, int D, int G, int PASS>
 struct ScoreTile {
@@ -161,16 +213,24 @@ struct ScoreTile {
   bool tile_base, tile_mixed, wg_base;
   float *xbuf, *ired, *obuf, *ibuf;
 
+  using KR = KeyRing<TT, D>;
   Frag<TT, D> qf[NB];
-  Frag<TT, D> kr[kPrefetch];
-  f32x4 acc[2][NB];
-  float mref[NB][4], lsum[NB][4], nlse[NB][4];
+  Frag<TT, D> kf;                 // key fragment of the current step
+  uint4* ring;                    // this wave's LDS slots
+  __amdgpu_buffer_rsrc_t krsrc;   // keys [0, tend) of (b, h)
+  int kstride;                    // bytes between consecutive keys
+  int voff[KR::NI];               // byte offset of this lane's piece in each load
+  f32x4 acc[NB];
+  float mref[NB];  // pass 1: wave-uniform reference of each block
+  float lsum[NB][4], nlse[NB][4];
   int pos[RB][4];
 
   __device__ __forceinline__ ScoreTile(const Problem& P_, const ScoreIO& io_, int b_, int kt_,
                                        int rtg_, float* smem)
       : P(P_), io(io_), b(b_), kt(kt_), rtg(rtg_) {
-    const int w = threadIdx.x >> 6;
+    // wave-uniform by construction; readfirstlane lets the compiler keep the
+    // wave's head, tile and buffer resource in scalar registers
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     lane = threadIdx.x & 63;
     c = lane >> 4;
     n = lane & 15;
@@ -208,12 +268,20 @@ struct ScoreTile {
     ke = min(ks + tile, tend);
     lim_min = P.T - P.Wn + max(r_lo, 0);
     kbase = io.k + ((int64_t)b * io.ks_b + (int64_t)h * io.ks_h) * ES;
-    // Steps are padded to a multiple of the prefetch depth (and, in pass 2, of
-    // the importance exchange) so the unrolled loop has no step guard; keys at
-    // or past ke are masked (pass 1) or never stored (pass 2).
+    kstride = (int)(io.ks_t * ES);  // the host checks tend * kstride < 2^31
+    krsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(kbase), 0, tend * kstride, kBufferWord3);
+#pragma unroll
+    for (int i = 0; i < KR::NI; ++i) {
+      const int kin = i * KR::KPI + lane / KR::CPR;             // key within the step
+      const int piece = (lane % KR::CPR) ^ (kin & KR::SWZ);     // stored at lane % CPR
+      voff[i] = kin * kstride + piece * 16;
+    }
+    ring = reinterpret_cast<uint4*>(smem) + w * (KR::R * KR::SLOT / 16);
+    // In pass 2 the steps are padded to the importance exchange; keys at or
+    // past ke are masked (pass 1) or never stored (pass 2), and keys past tend
+    // read as zero.
     nsteps = (ke - ks + 15) / 16;
-    const int sub = PASS == 2 ? max(kPrefetch, P.SK / 16) : kPrefetch;
-    nsteps = (nsteps + sub - 1) / sub * sub;
+    if constexpr (PASS == 2) nsteps = (nsteps + P.SK / 16 - 1) / (P.SK / 16) * (P.SK / 16);
 
     tile_base = tile_mixed = wg_base = false;
     if constexpr (PASS == 1) {
@@ -242,25 +310,29 @@ struct ScoreTile {
     rr0 = max(0, base_lo - r_lo);
     // pass-2 LDS per tile slot: importance exchange, its reduction, the staged
     // per-key sums of each head, and the staged importance of the key tile
-    xbuf = smem + slot * (P.H * WR * P.SK + 64 * P.H + 2 * P.H * kTile2 + kTile2);
+    xbuf = smem + key_ring_bytes(ES, D) / 4 + slot * (P.H * WR * P.SK + 64 * P.H + 2 * P.H * kTile2 + kTile2);
     ired = xbuf + P.H * WR * P.SK;
     obuf = ired + 64 * P.H;
     ibuf = obuf + 2 * P.H * kTile2;
   }
 
-  __device__ __forceinline__ void load_keys(int u, int step) {
-    // unconditional: rows clamped to tend-1 (masked or never stored)
-    const int t = min(ks + 16 * step + n, tend - 1);
-    kr[u].load(kbase + (int64_t)t * io.ks_t * ES, c);
-  }
-
-  template <int SET, int RING>
-  __device__ __forceinline__ void mma_step() {
+  // Copy the 16 keys of step st into ring slot u (lane l writes 16 bytes at
+  // l * 16 of each 1 KiB load; its global piece is pre-swizzled in voff).
+  __device__ __forceinline__ void dma(int u, int st) {
+    auto* dst = (__attribute__((address_space(3))) char*)(reinterpret_cast<char*>(ring) + u * KR::SLOT);
+    const int soff = (ks + 16 * st) * kstride;
 #pragma unroll
-    for (int bk = 0; bk < NB; ++bk) acc[SET][bk] = mma<D>(qf[bk], kr[RING], f32x4{0.f, 0.f, 0.f, 0.f});
+    for (int i = 0; i < KR::NI; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, voff[i], soff, 0, 0);
   }
 
-  template <int SET, bool MASKED>
+  __device__ __forceinline__ void mma_slot(int u) {
+    kf.load_lds(ring + u * (KR::SLOT / 16), n, c, KR::SWZ);
+#pragma unroll
+    for (int bk = 0; bk < NB; ++bk) acc[bk] = mma<D>(qf[bk], kf, f32x4{0.f, 0.f, 0.f, 0.f});
+  }
+
+  template <bool MASKED>
   __device__ __forceinline__ void epilogue(int s) {
     const int t = ks + 16 * s + n;
     if constexpr (PASS == 1) {
@@ -269,7 +341,7 @@ struct ScoreTile {
         const int rb = bk % RB;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float x = fmaf(acc[SET][bk][i], P.sc, -mref[bk][i]);
+          float x = fmaf(acc[bk][i], P.sc, -mref[bk]);
           if constexpr (MASKED) x = (t <= pos[rb][i] && t < ke) ? x : -INFINITY;
           lsum[bk][i] += __builtin_amdgcn_exp2f(x);
         }
@@ -285,7 +357,7 @@ struct ScoreTile {
         const int rb = bk % RB;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float p = __builtin_amdgcn_exp2f(fmaf(acc[SET][bk][i], P.sc, nlse[bk][i]));
+          float p = __builtin_amdgcn_exp2f(fmaf(acc[bk][i], P.sc, nlse[bk][i]));
           if constexpr (MASKED) p = t <= pos[rb][i] ? p : 0.f;
           gs[rb][i] += p;
         }
@@ -346,63 +418,73 @@ struct ScoreTile {
     lds_barrier();
   }
 
-  // One step of the software pipeline: the MFMAs of step s+1 are issued into
-  // the other accumulator set before the epilogue of step s, so matrix cores
-  // and vector ALU work concurrently; then ring slot U (step s, already
-  // consumed) is refilled with step s + kPrefetch.
-  template <int U, bool TILE_MASKED>
-  __device__ __forceinline__ void step(int s) {
-    constexpr int CUR = kPipelineMma ? (U & 1) : 0, NXT = CUR ^ 1;
-    if constexpr (kPipelineMma) {
-      if (s + 1 < nsteps) mma_step<NXT, (U + 1) % kPrefetch>();
+  // One step: refill the slot read by the previous step with step s + R - 1,
+  // wait for step s's keys, then its products and exponentials.
+  template <bool TILE_MASKED>
+  __device__ __forceinline__ void step(int s, int u) {
+    if constexpr (KR::R > 1) {
+      dma(u == 0 ? KR::R - 1 : u - 1, s + KR::R - 1);
+      wait_vmem<(KR::R - 1) * KR::NI>();
     } else {
-      mma_step<0, U>();
+      dma(0, s);
+      wait_vmem<0>();
     }
-    load_keys(U, s + kPrefetch);
+    mma_slot(u);
     if constexpr (TILE_MASKED) {
       const int t0 = ks + 16 * s;
       if (t0 + 15 > lim_min || (PASS == 1 && t0 + 16 > ke))
-        epilogue<CUR, true>(s);
+        epilogue<true>(s);
       else
-        epilogue<CUR, false>(s);
+        epilogue<false>(s);
     } else {
-      epilogue<CUR, false>(s);
+      epilogue<false>(s);
     }
     if constexpr (PASS == 2) {
       if (wg_base && ((s + 1) * 16) % P.SK == 0) exchange(s);
     }
+    // The next step's slot reads must not move above this step's work.
+    __builtin_amdgcn_sched_barrier(0);
   }
 
   template <bool TILE_MASKED>
   __device__ __forceinline__ void run() {
-    for (int s0 = 0; s0 < nsteps; s0 += kPrefetch) {
-      static_assert(kPrefetch == 4, "the step sequence below assumes four ring slots");
-      step<0, TILE_MASKED>(s0);
-      step<1, TILE_MASKED>(s0 + 1);
-      step<2, TILE_MASKED>(s0 + 2);
-      step<3, TILE_MASKED>(s0 + 3);
+    int u = 0;
+    for (int s = 0; s < nsteps; ++s) {
+      step<TILE_MASKED>(s, u);
+      u = u + 1 == KR::R ? 0 : u + 1;
     }
   }
 
   __device__ __forceinline__ void execute() {
+    // The ring starts with steps 0..R-2 in flight; step s issues s + R - 1
+    // into the slot step s - 1 has finished reading.
 #pragma unroll
-    for (int u = 0; u < kPrefetch; ++u) load_keys(u, u);
+    for (int u = 0; u + 1 < KR::R; ++u) dma(u, u);
     if constexpr (PASS == 1) {
-      mma_step<0, 0>();
-      // Reference of each (lane, row): its logit at the first key it sees; an
-      // invalid first key leaves -inf, and then every later key of that lane
-      // and row is masked too (keys only grow).
+      // Block references from the first 16 keys (recomputed by step 0).  A
+      // row with any valid key in this tile sees the tile's first key, so a
+      // block is -inf only when none of its rows has a valid key here.
+      if constexpr (KR::R > 1) {
+        wait_vmem<(KR::R - 2) * KR::NI>();
+      } else {
+        dma(0, 0);
+        wait_vmem<0>();
+      }
+      mma_slot(0);
       const int t = ks + n;
-      const bool m0 = ks + 15 > lim_min || ks + 16 > ke;
 #pragma unroll
-      for (int bk = 0; bk < NB; ++bk)
+      for (int bk = 0; bk < NB; ++bk) {
+        float m = -INFINITY;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const bool valid = !m0 || (t <= pos[bk % RB][i] && t < ke);
-          mref[bk][i] = valid ? acc[0][bk][i] * P.sc : -INFINITY;
+          const bool real = r_lo + (bk % RB) * 16 + 4 * c + i >= 0;  // not a padding row
+          const bool valid = real && t <= pos[bk % RB][i] && t < ke;
+          m = fmaxf(m, valid ? acc[bk][i] * P.sc : -INFINITY);
         }
-    } else if constexpr (kPipelineMma) {
-      mma_step<0, 0>();
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
+        mref[bk] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(m)));
+      }
     }
     // Only tiles that reach the causal edge, T or their own end need masks;
     // every other tile runs a loop without any masking code.
@@ -434,22 +516,21 @@ struct ScoreTile {
         }
       }
     } else {
-      // A lane whose later logits exceed its reference by more than the fp32
-      // exponent range leaves a non-finite sum; the row-normaliser task then
-      // recomputes that tile's partial with the exact online recurrence.
 #pragma unroll
       for (int bk = 0; bk < NB; ++bk) {
         const int g = bk / RB, rb = bk % RB;
         const int j = h * G + g;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float m = mref[bk][i], l = lsum[bk][i];
+          float l = lsum[bk][i];
 #pragma unroll
-          for (int o = 1; o < 16; o <<= 1) {
-            const float m2 = __shfl_xor(m, o), l2 = __shfl_xor(l, o);
-            lse_merge(m, l, m2, l2);
-          }
+          for (int o = 1; o < 16; o <<= 1) l += __shfl_xor(l, o);
           const int r = r_lo + rb * 16 + 4 * c + i;
+          // rows past the tile's first key hold no valid key here: (-inf, 0)
+          const bool has_keys = ks <= pos[rb][i];
+          float m = has_keys ? mref[bk] : -INFINITY;
+          if (!has_keys) l = 0.f;
+          else if (!(l >= 0x1p-64f && l < INFINITY)) l = INFINITY;  // exact recompute
           if (active && n == 0 && r >= 0)
             io.lse_part[(((int64_t)b * P.HQ + j) * P.Wn + r) * P.n_kt1 + kt] = make_float2(m, l);
         }
