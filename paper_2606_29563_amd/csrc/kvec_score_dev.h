@@ -125,6 +125,63 @@ __device__ __forceinline__ f32x4 mma(const Frag<F32, D>& a, const Frag<F32, D>& 
 template <class TT>
 constexpr int elem_bytes() { return __is_same(TT, BF16) ? 2 : 4; }
 
+// Cross-lane reductions on DPP and the gfx950 lane-swap instructions (VALU
+// only, no LDS round trip).  A DPP row is 16 lanes: the lanes of one MFMA
+// output column group.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppSwap1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppSwap2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+
+// Sum over the 16 lanes of each row; every lane of the row gets the same sum.
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dpp_f<kDppSwap1>(v);
+  v += dpp_f<kDppSwap2>(v);
+  v += dpp_f<kDppHalfMirror>(v);
+  v += dpp_f<kDppMirror>(v);
+  return v;
+}
+__device__ __forceinline__ float row_max16(float v) {
+  v = fmaxf(v, dpp_f<kDppSwap1>(v));
+  v = fmaxf(v, dpp_f<kDppSwap2>(v));
+  v = fmaxf(v, dpp_f<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f<kDppMirror>(v));
+  return v;
+}
+// v_permlane32_swap / v_permlane16_swap exchange the upper half-wave (odd
+// rows) of a with the lower half-wave (even rows) of b.  Written out: the
+// compiler's builtin returns the first register for both results.  The s_nop
+// covers the wait states after the VALU writes of a and b.
+__device__ __forceinline__ void lane_swap32(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void lane_swap16(float& a, float& b) {
+  asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+// Sum of lanes l, l^16, l^32, l^48 (the four rows of a column), in every lane.
+__device__ __forceinline__ float col_sum4(float v) {
+  float a = v, b = v;
+  lane_swap32(a, b);  // a = v[l mod 32], b = v[l mod 32 + 32]
+  v = a + b;
+  a = v;
+  b = v;
+  lane_swap16(a, b);  // a = even row of the pair, b = odd row
+  return a + b;
+}
+__device__ __forceinline__ float col_max4(float v) {
+  float a = v, b = v;
+  lane_swap32(a, b);
+  v = fmaxf(a, b);
+  a = v;
+  b = v;
+  lane_swap16(a, b);
+  return fmaxf(a, b);
+}
+
 // Wait until at most N vector memory operations of this wave are pending.
 // Direct global-to-LDS loads are not tracked by the compiler's own waits, so
 // the key ring waits explicitly; the asm statement also keeps LDS reads from
@@ -215,7 +272,7 @@ struct ScoreTile {
 
   using KR = KeyRing<TT, D>;
   Frag<TT, D> qf[NB];
-  Frag<TT, D> kf;                 // key fragment of the current step
+  Frag<TT, D> kf[2];              // key fragments of the current and next step
   uint4* ring;                    // this wave's LDS slots
   __amdgpu_buffer_rsrc_t krsrc;   // keys [0, tend) of (b, h)
   int kstride;                    // bytes between consecutive keys
@@ -242,21 +299,6 @@ struct ScoreTile {
     r_lo = P.Wn - (rt + 1) * WR;  // lowest window row of this tile (may be < 0)
     base_lo = P.Wn - P.O;         // first row of the last-O window
 
-    // Query fragments; loads are unconditional (clamped rows) so the compiler
-    // can count outstanding loads exactly, then padding rows are zeroed.
-#pragma unroll
-    for (int bk = 0; bk < NB; ++bk) {
-      const int g = bk / RB, rb = bk % RB;
-      const int r = r_lo + rb * 16 + n;
-      const int j = h * G + g;
-      qf[bk].load(io.q + ((int64_t)b * io.qs_b + (int64_t)j * io.qs_h + (int64_t)max(r, 0) * io.qs_r) * ES,
-                  c);
-    }
-#pragma unroll
-    for (int bk = 0; bk < NB; ++bk) {
-      const int r = r_lo + (bk % RB) * 16 + n;
-      if (!(active && r >= 0)) qf[bk].zero();
-    }
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -277,11 +319,13 @@ struct ScoreTile {
       voff[i] = kin * kstride + piece * 16;
     }
     ring = reinterpret_cast<uint4*>(smem) + w * (KR::R * KR::SLOT / 16);
-    // In pass 2 the steps are padded to the importance exchange; keys at or
-    // past ke are masked (pass 1) or never stored (pass 2), and keys past tend
-    // read as zero.
+    // Steps are padded to an even count (the loop alternates two fragment
+    // registers) and, in pass 2, to the importance exchange; keys at or past
+    // ke are masked (pass 1) or never stored (pass 2), and keys past tend read
+    // as zero.
     nsteps = (ke - ks + 15) / 16;
-    if constexpr (PASS == 2) nsteps = (nsteps + P.SK / 16 - 1) / (P.SK / 16) * (P.SK / 16);
+    const int pad = PASS == 2 ? max(2, P.SK / 16) : 2;
+    nsteps = (nsteps + pad - 1) / pad * pad;
 
     tile_base = tile_mixed = wg_base = false;
     if constexpr (PASS == 1) {
@@ -316,6 +360,20 @@ struct ScoreTile {
     ibuf = obuf + 2 * P.H * kTile2;
   }
 
+  // Query fragments.  Padding rows (r < 0) load row 0 and inactive waves
+  // load their clamped rows: neither is ever stored, pass 1 leaves padding
+  // rows out of the block references and pass 2 gives them a zero weight.
+  __device__ __forceinline__ void load_queries() {
+#pragma unroll
+    for (int bk = 0; bk < NB; ++bk) {
+      const int g = bk / RB, rb = bk % RB;
+      const int r = r_lo + rb * 16 + n;
+      const int j = h * G + g;
+      qf[bk].load(io.q + ((int64_t)b * io.qs_b + (int64_t)j * io.qs_h + (int64_t)max(r, 0) * io.qs_r) * ES,
+                  c);
+    }
+  }
+
   // Copy the 16 keys of step st into ring slot u (lane l writes 16 bytes at
   // l * 16 of each 1 KiB load; its global piece is pre-swizzled in voff).
   __device__ __forceinline__ void dma(int u, int st) {
@@ -326,10 +384,15 @@ struct ScoreTile {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, voff[i], soff, 0, 0);
   }
 
-  __device__ __forceinline__ void mma_slot(int u) {
-    kf.load_lds(ring + u * (KR::SLOT / 16), n, c, KR::SWZ);
+  template <int F>
+  __device__ __forceinline__ void read_frag(int u) {
+    kf[F].load_lds(ring + u * (KR::SLOT / 16), n, c, KR::SWZ);
+  }
+
+  template <int F>
+  __device__ __forceinline__ void mma_frag() {
 #pragma unroll
-    for (int bk = 0; bk < NB; ++bk) acc[bk] = mma<D>(qf[bk], kf, f32x4{0.f, 0.f, 0.f, 0.f});
+    for (int bk = 0; bk < NB; ++bk) acc[bk] = mma<D>(qf[bk], kf[F], f32x4{0.f, 0.f, 0.f, 0.f});
   }
 
   template <bool MASKED>
@@ -371,10 +434,8 @@ struct ScoreTile {
           if (tile_mixed) s_base += (r_lo + rb * 16 + 4 * c + i >= base_lo) ? gs[rb][i] : 0.f;
         }
       if (tile_base && !tile_mixed) s_base = s_all;
-      s_all += __shfl_xor(s_all, 16);
-      s_all += __shfl_xor(s_all, 32);
-      s_base += __shfl_xor(s_base, 16);
-      s_base += __shfl_xor(s_base, 32);
+      s_all = col_sum4(s_all);
+      s_base = col_sum4(s_base);
       // Stage the per-key sums in LDS; they are written out after the loop so
       // that the loop issues no global stores (exact load counting).
       if (c == 0) {
@@ -418,18 +479,23 @@ struct ScoreTile {
     lds_barrier();
   }
 
-  // One step: refill the slot read by the previous step with step s + R - 1,
-  // wait for step s's keys, then its products and exponentials.
-  template <bool TILE_MASKED>
+  // Key steps in flight ahead of the one being read: step s + kAhead is
+  // issued at step s into slot (s + kAhead) mod R, whose previous step was
+  // read at step s + kAhead - R - 1 < s.
+  static constexpr int kAhead = KR::R > 1 ? KR::R - 1 : 1;
+
+  // One step: the products of step s (fragment F, read during step s - 1),
+  // then the copy of step s + kAhead, the read of step s + 1's fragment once
+  // its copy has landed, and the exponentials of step s while that read is in
+  // flight.  u is the slot of step s + 1.
+  template <int F, bool TILE_MASKED>
   __device__ __forceinline__ void step(int s, int u) {
-    if constexpr (KR::R > 1) {
-      dma(u == 0 ? KR::R - 1 : u - 1, s + KR::R - 1);
-      wait_vmem<(KR::R - 1) * KR::NI>();
-    } else {
-      dma(0, s);
-      wait_vmem<0>();
-    }
-    mma_slot(u);
+    mma_frag<F>();
+    const int ua = KR::R > 1 ? (u + kAhead - 1) % KR::R : 0;
+    dma(ua, s + kAhead);
+    wait_vmem<(kAhead - 1) * KR::NI>();
+    read_frag<F ^ 1>(u);
+    __builtin_amdgcn_sched_barrier(0);  // issue the reads before the exponentials
     if constexpr (TILE_MASKED) {
       const int t0 = ks + 16 * s;
       if (t0 + 15 > lim_min || (PASS == 1 && t0 + 16 > ke))
@@ -442,35 +508,39 @@ struct ScoreTile {
     if constexpr (PASS == 2) {
       if (wg_base && ((s + 1) * 16) % P.SK == 0) exchange(s);
     }
-    // The next step's slot reads must not move above this step's work.
+    // Keep the steps in program order (the next step's waits stay after
+    // this step's work).
     __builtin_amdgcn_sched_barrier(0);
   }
 
   template <bool TILE_MASKED>
   __device__ __forceinline__ void run() {
-    int u = 0;
-    for (int s = 0; s < nsteps; ++s) {
-      step<TILE_MASKED>(s, u);
+    int u = KR::R > 1 ? 1 : 0;  // slot of step s + 1
+    for (int s = 0; s < nsteps; s += 2) {
+      step<0, TILE_MASKED>(s, u);
+      u = u + 1 == KR::R ? 0 : u + 1;
+      step<1, TILE_MASKED>(s + 1, u);
       u = u + 1 == KR::R ? 0 : u + 1;
     }
   }
 
   __device__ __forceinline__ void execute() {
-    // The ring starts with steps 0..R-2 in flight; step s issues s + R - 1
-    // into the slot step s - 1 has finished reading.
+    // Steps 0..kAhead-1 are in flight before the loop, the queries loaded
+    // right after step 0's keys (both long-latency), and step 0's fragment is
+    // read as soon as its copy and the queries have landed.
+    dma(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_queries();
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int u = 0; u + 1 < KR::R; ++u) dma(u, u);
+    for (int st = 1; st < kAhead; ++st) dma(st % KR::R, st);
+    wait_vmem<(kAhead - 1) * KR::NI>();
+    read_frag<0>(0);
     if constexpr (PASS == 1) {
       // Block references from the first 16 keys (recomputed by step 0).  A
       // row with any valid key in this tile sees the tile's first key, so a
       // block is -inf only when none of its rows has a valid key here.
-      if constexpr (KR::R > 1) {
-        wait_vmem<(KR::R - 2) * KR::NI>();
-      } else {
-        dma(0, 0);
-        wait_vmem<0>();
-      }
-      mma_slot(0);
+      mma_frag<0>();
       const int t = ks + n;
 #pragma unroll
       for (int bk = 0; bk < NB; ++bk) {
@@ -481,8 +551,7 @@ struct ScoreTile {
           const bool valid = real && t <= pos[bk % RB][i] && t < ke;
           m = fmaxf(m, valid ? acc[bk][i] * P.sc : -INFINITY);
         }
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o));
+        m = col_max4(row_max16(m));
         mref[bk] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(m)));
       }
     }
@@ -522,9 +591,7 @@ struct ScoreTile {
         const int j = h * G + g;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float l = lsum[bk][i];
-#pragma unroll
-          for (int o = 1; o < 16; o <<= 1) l += __shfl_xor(l, o);
+          float l = row_sum16(lsum[bk][i]);
           const int r = r_lo + rb * 16 + 4 * c + i;
           // rows past the tile's first key hold no valid key here: (-inf, 0)
           const bool has_keys = ks <= pos[rb][i];
