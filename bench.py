@@ -50,16 +50,22 @@ def _elapsed(hip, a, b) -> float:
     return ms.value
 
 
-def cpu_baseline(w, sample_layers: int):
-    """The oracle as it stands, on `sample_layers` layers of sequence 0."""
+def cpu_baseline(w, max_layers: int, min_seconds: float = 10.0):
+    """The oracle as it stands, timed on sequence 0 layer by layer in the
+    step's order (layer l uses the bitmaps of layers < l), until about
+    `min_seconds` of oracle work or `max_layers` layer evictions."""
     import numpy as np
     import threadpoolctl
 
     import oracle as orc
     import synth
     t_work = 0.0
+    done = 0
     prev = []
-    for l in range(sample_layers):
+    while done < max_layers and (done == 0 or t_work < min_seconds):
+        l = done % w.n_layers
+        if l == 0:
+            prev = []
         q = synth.to_f64(synth.queries(w, l, 0), w.dtype)
         k = synth.to_f64(synth.keys(w, l, 0), w.dtype)
         v = synth.values(w, l, 0)
@@ -71,13 +77,15 @@ def cpu_baseline(w, sample_layers: int):
         orc.gather_rows(v, res.idx)
         t_work += time.perf_counter() - t0
         prev.append(res.bits)
-    per_layer = t_work / sample_layers
+        done += 1
+    per_layer = t_work / done
     step_s = per_layer * w.n_layers * w.batch
     threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
     return {"value": w.batch * w.seq_len / step_s, "unit": "prefix tokens/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{sample_layers} of {w.n_layers} layers of sequence 0 "
-                      f"({t_work:.1f} s); extrapolated to {w.n_layers} layers x batch {w.batch}"}
+            "sample": f"{done} layer evictions of sequence 0 in layer order ({t_work:.1f} s of "
+                      f"oracle work, input generation excluded); per-layer time extrapolated "
+                      f"to {w.n_layers} layers x batch {w.batch}"}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "step_kernel_{workload}_traffic.md")
@@ -219,8 +227,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        # about 10 s of oracle work (~5e-5 s per token and layer on 8 cores)
-        sample = args.cpu_sample_layers or max(1, min(L, round(10.0 / (5e-5 * T))))
+        # layers of sequence 0 in order until about 10 s of oracle work
+        sample = args.cpu_sample_layers or 4 * L
         print(f"[bench] CPU oracle on {sample} layer(s)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, sample)
 
