@@ -63,16 +63,25 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   const int tpw = 8 / H;
   x.n_rtg = (x.n_rt + tpw - 1) / tpw;
   x.n_kt1 = (x.T + kTile1 - 1) / kTile1;
-  x.n_kt2 = (x.Tc + kTile2 - 1) / kTile2;
-  // pass-2 LDS: the key ring plus, per row tile, the importance exchange
-  // (H * WR * SK), its reduction, the staged per-key sums and importance
+  // pass-2 LDS: the key ring plus, per row tile, the running max over heads
+  // (SK keys per exchange period), the staged per-key sums and importance of
+  // the key tile.  Prefer 512-key tiles (fewer work-groups, less fixed cost
+  // per key) with periods of at least 32 keys, then the widest period.
   const size_t ring = key_ring_bytes(c->dtype == KVEC_BF16 ? 2 : 4, x.D);
-  auto lds_p2 = [&](int sk) {
-    return ring + (size_t)tpw * ((size_t)H * x.WR * sk + 64 * H + 2 * H * kTile2 + kTile2) * 4;
+  auto lds_p2 = [&](int sk, int tile) {
+    return ring + (size_t)tpw * p2_slot_floats(H, x.WR, sk, tile) * 4;
   };
-  x.SK = 64;
-  while (x.SK > 16 && lds_p2(x.SK) > kLdsMax - kLdsStatic) x.SK /= 2;
-  if (lds_p2(x.SK) > kLdsMax - kLdsStatic) return KVEC_ERR_UNSUPPORTED;
+  const size_t lds_cap = kLdsMax - kLdsStatic;
+  x.tile2 = 0;
+  for (int tile = kTile2Max; tile >= kTile2Max / 2 && !x.tile2; tile /= 2)
+    for (int sk = 128; sk >= (tile == kTile2Max ? 32 : 16); sk /= 2)
+      if (lds_p2(sk, tile) <= lds_cap) {
+        x.tile2 = tile;
+        x.SK = sk;
+        break;
+      }
+  if (!x.tile2) return KVEC_ERR_UNSUPPORTED;
+  x.n_kt2 = (x.Tc + x.tile2 - 1) / x.tile2;
   x.n_pool = (x.Tc + kPoolChunk - 1) / kPoolChunk;
   x.n_prep = (x.Tc + kPrepChunk - 1) / kPrepChunk;
   x.words = (x.T + 63) / 64;
@@ -124,7 +133,7 @@ Workspace make_workspace(const Geometry& g) {
   const int tpw = 8 / P.H;
   const size_t lds_p2 =
       key_ring_bytes(P.esize, P.D) +
-      (size_t)tpw * ((size_t)P.H * P.WR * P.SK + 64 * P.H + 2 * P.H * kTile2 + kTile2) * 4;
+      (size_t)tpw * p2_slot_floats(P.H, P.WR, P.SK, P.tile2) * 4;
   const size_t lds_pool = (size_t)(2 * (kPoolChunk + 64) + 2 * kHistBins) * 4 + 16 * 8;
   const size_t lds_prep = 256;
   const size_t lds_sel = 2048 * 4 + 32 * 4 + (size_t)((P.n_prep + 1 + 3) & ~3) * 4 +

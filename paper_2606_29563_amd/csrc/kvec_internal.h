@@ -13,7 +13,7 @@ constexpr int kThreads = 512;  // every work-group of the step kernel: 8 waves
 constexpr int kRing = 6;       // layers in flight in the software pipeline
 
 constexpr int kTile1 = 512;       // keys per pass-1 work-group
-constexpr int kTile2 = 256;       // keys per pass-2 work-group
+constexpr int kTile2Max = 512;    // keys per pass-2 work-group (512 or 256, by LDS)
 constexpr int kPoolChunk = 1024;  // tokens per pool task
 constexpr int kPrepChunk = 1024;  // tokens per prep task
 constexpr int kHistBits = 12;     // selection histograms over the top 12 key bits
@@ -40,12 +40,18 @@ constexpr int key_ring_slots(int esize, int D) {
 constexpr size_t key_ring_bytes(int esize, int D) {
   return (size_t)(kThreads / 64) * key_ring_slots(esize, D) * 16 * D * esize;
 }
+// Pass-2 LDS floats per row-tile slot: two running-max buffers [WR][SK + 4]
+// (only with more than one head), per-key sums of each head (base and all
+// rows) and the importance of the key tile.
+__host__ __device__ constexpr int p2_slot_floats(int H, int WR, int SK, int tile2) {
+  return (H > 1 ? 2 * WR * (SK + 4) : 0) + 2 * H * tile2 + tile2;
+}
 
 // Problem geometry visible to device code.
 struct Problem {
   int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;
   float lam, sc, inv_go, inv_gwn;
-  int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK;
+  int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK, tile2;
   int n_pool, n_prep, words;
   int esize;
   int n_gather;  // gather work-groups per (layer, sequence)

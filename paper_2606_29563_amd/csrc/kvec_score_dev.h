@@ -182,6 +182,14 @@ __device__ __forceinline__ float col_max4(float v) {
   return fmaxf(a, b);
 }
 
+// LDS atomic max without return.  Written out: for the builtin the compiler
+// first drains every direct-to-LDS load in flight (it cannot tell the
+// addresses apart), which would stall the key ring at every step.
+__device__ __forceinline__ void lds_max_u32(unsigned* p, unsigned v) {
+  const auto* lp = (__attribute__((address_space(3))) unsigned*)p;
+  asm volatile("ds_max_u32 %0, %1" ::"v"(lp), "v"(v) : "memory");
+}
+
 // Wait until at most N vector memory operations of this wave are pending.
 // Direct global-to-LDS loads are not tracked by the compiler's own waits, so
 // the key ring waits explicitly; the asm statement also keeps LDS reads from
@@ -268,7 +276,7 @@ struct ScoreTile {
   int r_lo, base_lo, tend, ks, ke, lim_min, nsteps, rr0;
   const char* kbase;
   bool tile_base, tile_mixed, wg_base;
-  float *xbuf, *ired, *obuf, *ibuf;
+  float *mbuf, *obuf, *ibuf;
 
   using KR = KeyRing<TT, D>;
   Frag<TT, D> qf[NB];
@@ -305,7 +313,7 @@ struct ScoreTile {
       for (int i = 0; i < 4; ++i) pos[rb][i] = P.T - P.Wn + (r_lo + rb * 16 + 4 * c + i);
 
     tend = PASS == 1 ? P.T : P.Tc;
-    const int tile = PASS == 1 ? kTile1 : kTile2;
+    const int tile = PASS == 1 ? kTile1 : P.tile2;
     ks = kt * tile;
     ke = min(ks + tile, tend);
     lim_min = P.T - P.Wn + max(r_lo, 0);
@@ -352,12 +360,12 @@ struct ScoreTile {
       wg_base = (P.Wn - (rtg * tpw + 1) * WR) + WR > base_lo;
     }
     rr0 = max(0, base_lo - r_lo);
-    // pass-2 LDS per tile slot: importance exchange, its reduction, the staged
+    // pass-2 LDS per tile slot (after the key rings): two buffers of the
+    // running max over heads [WR][SK + 4] (none for one head), the staged
     // per-key sums of each head, and the staged importance of the key tile
-    xbuf = smem + key_ring_bytes(ES, D) / 4 + slot * (P.H * WR * P.SK + 64 * P.H + 2 * P.H * kTile2 + kTile2);
-    ired = xbuf + P.H * WR * P.SK;
-    obuf = ired + 64 * P.H;
-    ibuf = obuf + 2 * P.H * kTile2;
+    mbuf = smem + key_ring_bytes(ES, D) / 4 + slot * p2_slot_floats(P.H, WR, P.SK, P.tile2);
+    obuf = mbuf + (P.H > 1 ? 2 * WR * (P.SK + 4) : 0);
+    ibuf = obuf + 2 * P.H * P.tile2;
   }
 
   // Query fragments.  Padding rows (r < 0) load row 0 and inactive waves
@@ -439,44 +447,49 @@ struct ScoreTile {
       // Stage the per-key sums in LDS; they are written out after the loop so
       // that the loop issues no global stores (exact load counting).
       if (c == 0) {
-        obuf[(h * 2 + 0) * kTile2 + s * 16 + n] = s_all;
-        obuf[(h * 2 + 1) * kTile2 + s * 16 + n] = s_base;
+        obuf[(h * 2 + 0) * P.tile2 + s * 16 + n] = s_all;
+        obuf[(h * 2 + 1) * P.tile2 + s * 16 + n] = s_base;
       }
-      if (wg_base && tile_base) {
-        const int kk = (s * 16) % P.SK + n;
+      if (tile_base) {
+        if (P.H == 1) {
+          // one head: the max over heads is the head itself
+          if (c == 0) ibuf[s * 16 + n] = s_base;
+        } else {
+          // running max over the heads of this slot: p >= 0, so the float
+          // order is the order of the bit patterns (ds_max_u32)
+          const int kk = (s * 16) % P.SK + n;
+          unsigned* mb = reinterpret_cast<unsigned*>(mbuf) + (((s * 16) / P.SK) & 1) * WR * (P.SK + 4);
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
+          for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int rr = rb * 16 + 4 * c + i;
-            if (rr >= rr0) xbuf[(h * WR + rr) * P.SK + kk] = gs[rb][i];
-          }
+            for (int i = 0; i < 4; ++i) {
+              const int rr = rb * 16 + 4 * c + i;
+              if (rr >= rr0) lds_max_u32(mb + rr * (P.SK + 4) + kk, __float_as_uint(gs[rb][i]));
+            }
+        }
       }
     }
   }
 
-  // Importance of one exchange block: max over heads, then sum over base rows.
+  // End of an exchange period of SK keys (step s is its last): once every
+  // head of the slot has folded its rows in, one wave of the slot (rotating)
+  // sums the maxima over the rows into the importance of those keys and
+  // clears the buffer, which is written again two periods later, after the
+  // next period's barrier.
   __device__ __forceinline__ void exchange(int s) {
     lds_barrier();
-    const int nthr = 64 * P.H;
-    const int ts = threadIdx.x - slot * nthr;  // thread index within the slot
-    if (tile_base && slot < tpw) {
-      const int kcol = ts % P.SK, rg = ts / P.SK, nrg = nthr / P.SK;
-      float acc_i = 0.f;
-      for (int rr = rr0 + rg; rr < WR; rr += nrg) {
-        float m = xbuf[rr * P.SK + kcol];
-        for (int hh = 1; hh < P.H; ++hh) m = fmaxf(m, xbuf[(hh * WR + rr) * P.SK + kcol]);
-        acc_i += m;
+    const int period = (s * 16) / P.SK;
+    if (tile_base && h == period % P.H) {
+      float* mb = mbuf + (period & 1) * WR * (P.SK + 4);
+      for (int kc = lane; kc < P.SK; kc += 64) {
+        float v = 0.f;
+        for (int rr = 0; rr < WR; ++rr) {  // rows before rr0 stay zero
+          v += mb[rr * (P.SK + 4) + kc];
+          mb[rr * (P.SK + 4) + kc] = 0.f;
+        }
+        ibuf[period * P.SK + kc] = v;
       }
-      ired[rg * P.SK + kcol] = acc_i;
     }
-    lds_barrier();
-    if (tile_base && slot < tpw && ts < P.SK) {
-      float v = 0.f;
-      for (int g2 = 0; g2 < nthr / P.SK; ++g2) v += ired[g2 * P.SK + ts];
-      ibuf[(s + 1) * 16 - P.SK + ts] = v;
-    }
-    lds_barrier();
   }
 
   // Key steps in flight ahead of the one being read: step s + kAhead is
@@ -506,7 +519,7 @@ struct ScoreTile {
       epilogue<false>(s);
     }
     if constexpr (PASS == 2) {
-      if (wg_base && ((s + 1) * 16) % P.SK == 0) exchange(s);
+      if (wg_base && P.H > 1 && ((s + 1) * 16) % P.SK == 0) exchange(s);
     }
     // Keep the steps in program order (the next step's waits stay after
     // this step's work).
@@ -525,6 +538,13 @@ struct ScoreTile {
   }
 
   __device__ __forceinline__ void execute() {
+    if constexpr (PASS == 2) {
+      // clear both running-max buffers before any head folds rows in
+      if (wg_base && P.H > 1) {
+        for (int i = lane + (h % P.H) * 64; i < 2 * WR * (P.SK + 4); i += 64 * P.H) mbuf[i] = 0.f;
+        lds_barrier();
+      }
+    }
     // Steps 0..kAhead-1 are in flight before the loop, the queries loaded
     // right after step 0's keys (both long-latency), and step 0's fragment is
     // read as soon as its copy and the queries have landed.
@@ -570,15 +590,15 @@ struct ScoreTile {
       lds_barrier();
       if (active) {
         const int64_t o = (((int64_t)b * P.n_rt + rt) * P.H + h) * P.Tc;
-        for (int i = lane; i < kTile2; i += 64) {
+        for (int i = lane; i < P.tile2; i += 64) {
           const int t = ks + i;
           if (t < P.Tc) {
-            io.psum_all[o + t] = obuf[(h * 2 + 0) * kTile2 + i];
-            io.psum_base[o + t] = obuf[(h * 2 + 1) * kTile2 + i];
+            io.psum_all[o + t] = obuf[(h * 2 + 0) * P.tile2 + i];
+            io.psum_base[o + t] = obuf[(h * 2 + 1) * P.tile2 + i];
           }
         }
         if (tile_base && h == 0) {
-          for (int i = lane; i < kTile2; i += 64) {
+          for (int i = lane; i < P.tile2; i += 64) {
             const int t = ks + i;
             if (t < P.Tc) io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t] = ibuf[i];
           }
