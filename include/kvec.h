@@ -165,7 +165,7 @@ kvec_status kvec_evict_model(const kvec_config* cfg,
                              hipEvent_t* events);
 
 /* Number of events kvec_evict_model records when given an event array
- * (n_layers + 7; 0 when T <= B), or -1 for an invalid configuration. */
+ * (n_layers + 11; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);
 
 /* Coverage C (Sec. 3.2) per sequence over layers 0..upto_layer:

@@ -68,8 +68,16 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   // the key tile.  Prefer 512-key tiles (fewer work-groups, less fixed cost
   // per key) with periods of at least 32 keys, then the widest period.
   const size_t ring = key_ring_bytes(c->dtype == KVEC_BF16 ? 2 : 4, x.D);
+  // row tiles of the layer pipeline: the last-O rows for every head, the
+  // remaining extended-window rows for the delta_eff heads of H_top
+  x.n_rtg_base = (x.n_rt_base + tpw - 1) / tpw;
+  const int n_rt_ext = x.n_rt - x.n_rt_base;
+  x.tpw_x = x.delta_eff > 0 ? 8 / x.delta_eff : 0;
+  x.n_rtg_x = x.delta_eff > 0 && n_rt_ext > 0 ? (n_rt_ext + x.tpw_x - 1) / x.tpw_x : 0;
   auto lds_p2 = [&](int sk, int tile) {
-    return ring + (size_t)tpw * p2_slot_floats(H, x.WR, sk, tile) * 4;
+    const size_t all = (size_t)tpw * p2_slot_floats(H, x.WR, sk, tile, H > 1);
+    const size_t ext = x.delta_eff > 0 ? (size_t)x.tpw_x * p2_slot_floats(x.delta_eff, x.WR, sk, tile, false) : 0;
+    return ring + (all > ext ? all : ext) * 4;
   };
   const size_t lds_cap = kLdsMax - kLdsStatic;
   x.tile2 = 0;
@@ -131,9 +139,10 @@ Workspace make_workspace(const Geometry& g) {
   w.total = off;
   // dynamic LDS: the largest task
   const int tpw = 8 / P.H;
-  const size_t lds_p2 =
-      key_ring_bytes(P.esize, P.D) +
-      (size_t)tpw * p2_slot_floats(P.H, P.WR, P.SK, P.tile2) * 4;
+  const size_t p2_all = (size_t)tpw * p2_slot_floats(P.H, P.WR, P.SK, P.tile2, P.H > 1);
+  const size_t p2_ext =
+      P.delta_eff > 0 ? (size_t)P.tpw_x * p2_slot_floats(P.delta_eff, P.WR, P.SK, P.tile2, false) : 0;
+  const size_t lds_p2 = key_ring_bytes(P.esize, P.D) + (p2_all > p2_ext ? p2_all : p2_ext) * 4;
   const size_t lds_pool = (size_t)(2 * (kPoolChunk + 64) + 2 * kHistBins) * 4 + 16 * 8;
   const size_t lds_prep = 256;
   const size_t lds_sel = 2048 * 4 + 32 * 4 + (size_t)((P.n_prep + 1 + 3) & ~3) * 4 +
@@ -342,7 +351,7 @@ kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, in
 int32_t kvec_profile_points(const kvec_config* cfg) {
   Geometry g;
   if (make_geometry(cfg, &g) != KVEC_OK) return -1;
-  return g.keep_all ? 0 : g.p.L + 7;
+  return g.keep_all ? 0 : g.p.L + kPipeDepth + 1;
 }
 
 const char* kvec_status_string(kvec_status s) {

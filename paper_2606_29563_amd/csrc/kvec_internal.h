@@ -10,12 +10,15 @@
 namespace kvec {
 
 constexpr int kThreads = 512;  // every work-group of the step kernel: 8 waves
-constexpr int kRing = 6;       // layers in flight in the software pipeline
+constexpr int kPipeDepth = 10;         // launches between a layer's first and last stage
+constexpr int kRing = kPipeDepth + 1;  // layers in flight in the software pipeline
 
 constexpr int kTile1 = 512;       // keys per pass-1 work-group
 constexpr int kTile2Max = 512;    // keys per pass-2 work-group (512 or 256, by LDS)
-constexpr int kPoolChunk = 1024;  // tokens per pool task
-constexpr int kPrepChunk = 1024;  // tokens per prep task
+constexpr int kPoolChunk = 1024;  // tokens per pool chunk
+constexpr int kPrepChunk = 1024;  // tokens per prep chunk (members are grouped per chunk)
+constexpr int kPoolPer = 4;       // pool chunks per pool work-group
+constexpr int kPrepPer = 8;       // prep chunks per prep work-group
 constexpr int kHistBits = 12;     // selection histograms over the top 12 key bits
 constexpr int kHistBins = 1 << kHistBits;
 
@@ -40,18 +43,27 @@ constexpr int key_ring_slots(int esize, int D) {
 constexpr size_t key_ring_bytes(int esize, int D) {
   return (size_t)(kThreads / 64) * key_ring_slots(esize, D) * 16 * D * esize;
 }
-// Pass-2 LDS floats per row-tile slot: two running-max buffers [WR][SK + 4]
-// (only with more than one head), per-key sums of each head (base and all
-// rows) and the importance of the key tile.
-__host__ __device__ constexpr int p2_slot_floats(int H, int WR, int SK, int tile2) {
-  return (H > 1 ? 2 * WR * (SK + 4) : 0) + 2 * H * tile2 + tile2;
+// Pass-2 LDS floats per row-tile slot of nh heads: two running-max buffers
+// [WR][SK + 4] when the slot exchanges the importance over heads, per-key
+// sums of each head (base and all rows) and the importance of the key tile.
+__host__ __device__ constexpr int p2_slot_floats(int nh, int WR, int SK, int tile2, bool exchange) {
+  return (exchange ? 2 * WR * (SK + 4) : 0) + 2 * nh * tile2 + tile2;
 }
+
+// Which window rows and heads a score pass covers.  ALL: every row tile and
+// head (the per-layer entry points).  BASE: the row tiles holding the last-O
+// rows, every head.  EXT: the remaining row tiles (rows of the extended window
+// only), for the heads of H_top only; their rows enter only P over O'.
+enum Part { PART_ALL = 0, PART_BASE = 1, PART_EXT = 2 };
 
 // Problem geometry visible to device code.
 struct Problem {
   int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;
   float lam, sc, inv_go, inv_gwn;
   int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK, tile2;
+  int n_rtg_base;  // work-groups per key tile of a BASE pass (8/H row tiles each)
+  int tpw_x;       // row tiles per work-group of an EXT pass (8 / delta_eff)
+  int n_rtg_x;     // work-groups per key tile of an EXT pass (0: no EXT pass)
   int n_pool, n_prep, words;
   int esize;
   int n_gather;  // gather work-groups per (layer, sequence)
@@ -107,6 +119,41 @@ hipError_t run_coverage(const Geometry& g, const uint64_t* bits, int upto, int64
 // ---------------------------------------------------------------------------
 // Device helpers
 // ---------------------------------------------------------------------------
+
+// H_top (Sec. 4.1): bit h set for the delta_eff heads of sequence b with the
+// lowest variance of pooled P (ties: lower head), from the per-chunk float64
+// sums of the pool stage.  Every caller computes it the same way, so the
+// score passes of the extended window and the selection agree.  Work-group
+// cooperative (barriers); `vars` holds 8 doubles of shared memory.
+__device__ __forceinline__ uint32_t htop_mask(const Problem& P, const double2* stats, int b,
+                                              double* vars) {
+  if ((int)threadIdx.x < P.H) {
+    const int g = threadIdx.x;
+    double a1 = 0.0, a2 = 0.0;
+    for (int i = 0; i < P.n_pool; ++i) {
+      const double2 v = stats[((int64_t)b * P.H + g) * P.n_pool + i];
+      a1 += v.x;
+      a2 += v.y;
+    }
+    const double mean = a1 / P.Tc;
+    vars[g] = a2 / P.Tc - mean * mean;
+  }
+  __syncthreads();
+  uint32_t m = 0;
+  for (int g = 0; g < P.H; ++g) {
+    int rank = 0;
+    for (int o = 0; o < P.H; ++o) rank += (vars[o] < vars[g]) || (vars[o] == vars[g] && o < g);
+    m |= (uint32_t)(rank < P.delta_eff) << g;
+  }
+  __syncthreads();
+  return m;
+}
+
+// Index of the k-th set bit of m, or -1 when m has at most k set bits.
+__device__ __forceinline__ int nth_bit(uint32_t m, int k) {
+  for (int i = 0; i < k; ++i) m &= m - 1u;
+  return __ffs(m) - 1;
+}
 
 // Order-preserving map of an IEEE float to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t float_key(float f) {

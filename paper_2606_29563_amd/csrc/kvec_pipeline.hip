@@ -2,22 +2,27 @@
 //
 // Every stage of one layer depends only on earlier stages of the same layer,
 // except the coverage-aware selection, which also needs the previous layer's
-// selection (its bitmap row defines n_t).  Launch j of the step therefore
-// runs, side by side in one grid of 512-thread work-groups:
+// selection (its bitmap row defines n_t).  The window rows split in two: the
+// last-O rows (P and I, every head) and the rest of the extended window (P
+// over O', needed only for the H_top heads, which are known once P is pooled).
+// Launch j of the step therefore runs, side by side in one grid of 512-thread
+// work-groups:
 //
-//   select  layer j-5   (one work-group per (sequence, head); the serial chain)
-//   count   layer j-5   (running coverage counts for the next selection)
-//   pass 1  layer j     (row-normaliser partials; K of layer j read from HBM)
-//   lse     layer j-1   (row normalisers from the partials)
-//   pass 2  layer j-2   (scores; K of layer j-2 re-read, resident in the
-//                        256 MB last-level cache since launch j-2)
-//   pool    layer j-3   (max-pool, statistics, histograms)
-//   prep    layer j-4   (sigma, H_top, candidate members)
-//   gather  layer j-6   (compacted cache)
+//   select   layer j-9   (one work-group per (sequence, head); the serial chain)
+//   count    layer j-9   (running coverage counts for the next selection)
+//   pass 2   layer j-2   last-O rows, every head: P, I
+//   pass 2   layer j-6   extended rows, H_top heads: the rest of P over O'
+//   pass 1   layer j     last-O rows: row-normaliser partials
+//   pass 1   layer j-4   extended rows of the H_top heads
+//   lse      layers j-1, j-5 (row normalisers of the two row sets)
+//   pool     layer j-3   P: max-pool, sigma sums, histogram, I
+//   pool     layer j-7   P over O' of the H_top heads
+//   prep     layer j-8   (sigma, H_top, candidate members)
+//   gather   layer j-10  (compacted cache)
 //
-// so L + 6 launches cover the whole step, each dominated by the two score
-// passes, and the serial selection chain runs in the shadow of the
-// HBM-bound scoring.  Per-layer scratch lives in a ring of kRing slots.
+// so L + 10 launches cover the whole step and the serial selection chain
+// runs in the shadow of the score passes.  Per-layer scratch lives in a ring
+// of kRing slots.
 //
 // Work-group IDs are dispatched round-robin over the 8 XCDs, each with its
 // own L2.  Within a stage, consecutive tasks (e.g. the row tiles of one key
@@ -31,7 +36,17 @@
 namespace kvec {
 namespace {
 
-enum Stage { ST_SELECT = 0, ST_COUNT, ST_PASS1, ST_LSE, ST_PASS2, ST_POOL, ST_PREP, ST_GATHER, ST_N };
+// Segments are dispatched in this order (long work-groups first).  *_B and
+// *_X are the last-O and the extended-window halves of the layer pipeline;
+// the plain stages cover every row and head (per-layer entry points).
+enum Stage {
+  ST_SELECT = 0, ST_COUNT,
+  ST_PASS2, ST_P2B, ST_P2X,
+  ST_PASS1, ST_P1B, ST_P1X,
+  ST_LSE, ST_LSEB, ST_LSEX,
+  ST_POOL, ST_POOLB, ST_POOLX,
+  ST_PREP, ST_GATHER, ST_N
+};
 
 struct Seg {
   int layer;  // model layer the stage works on
@@ -145,9 +160,20 @@ __device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b,
   }
 }
 
+// First window row held by the row tiles of the last-O rows.
+__host__ __device__ inline int base_row_lo(const Problem& P) { return max(0, P.Wn - P.n_rt_base * P.WR); }
+
+// Row-normaliser tasks per sequence of one LSE stage.
+__host__ __device__ inline int lse_tasks_per_seq(const Problem& P, int st) {
+  const int rb0 = base_row_lo(P);
+  const int nr = st == ST_LSEB ? P.Wn - rb0 : st == ST_LSEX ? rb0 : P.Wn;
+  return (P.HQ * nr + kLseRows - 1) / kLseRows;
+}
+
 template <class TT, int D, int G>
 __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
   extern __shared__ __align__(16) char smem[];
+  __shared__ double s_var[8];  // H_top of the extended-window stages
   const Problem P = a.P;
   int blk = blockIdx.x;
   int st = 0;
@@ -181,40 +207,85 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       task_count(P, prev, row, out, b, blk % parts);
       break;
     }
-    case ST_PASS1: {
-      const int per_b = P.n_kt1 * P.n_rtg;
+    case ST_PASS1:
+    case ST_P1B:
+    case ST_P1X: {
+      const Part part = st == ST_P1B ? PART_BASE : st == ST_P1X ? PART_EXT : PART_ALL;
+      const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
+      const int per_b = P.n_kt1 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
-      score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot), b, rem / P.n_rtg,
-                                     rem % P.n_rtg, reinterpret_cast<float*>(smem));
+      const uint32_t hm =
+          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b, s_var) : 0u;
+      score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot), b, rem / n_rtg, rem % n_rtg,
+                              reinterpret_cast<float*>(smem), part, hm);
       break;
     }
     case ST_LSE:
-      task_lse<TT, D, G>(P, score_io(a, sg.layer, sg.slot), blk);
+    case ST_LSEB:
+    case ST_LSEX: {
+      const int per_b = lse_tasks_per_seq(P, st);
+      const int b = blk / per_b;
+      const int rb0 = base_row_lo(P);
+      const uint32_t all = (1u << P.H) - 1u;
+      const ScoreIO io = score_io(a, sg.layer, sg.slot);
+      if (st == ST_LSE)
+        task_lse<TT, D, G>(P, io, b, blk % per_b, 0, P.Wn, all);
+      else if (st == ST_LSEB)
+        task_lse<TT, D, G>(P, io, b, blk % per_b, rb0, P.Wn - rb0, all);
+      else
+        task_lse<TT, D, G>(P, io, b, blk % per_b, 0, rb0,
+                           htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b, s_var));
       break;
-    case ST_PASS2: {
-      const int per_b = P.n_kt2 * P.n_rtg;
+    }
+    case ST_PASS2:
+    case ST_P2B:
+    case ST_P2X: {
+      const Part part = st == ST_P2B ? PART_BASE : st == ST_P2X ? PART_EXT : PART_ALL;
+      const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
+      const int per_b = P.n_kt2 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
       const ScoreIO io = score_io(a, sg.layer, sg.slot);
-      score_tile<TT, D, G, 2>(P, io, b, rem / P.n_rtg, rem % P.n_rtg,
-                                     reinterpret_cast<float*>(smem));
-      // Clear this sequence's histograms for the pool stage of this layer.
-      uint32_t* hist = reinterpret_cast<uint32_t*>(a.ws + (size_t)sg.slot * a.w.slot_bytes + a.w.hist) +
-                       (int64_t)b * 2 * P.H * kHistBins;
-      const int nwords = 2 * P.H * kHistBins;
-      const int per = (nwords + per_b - 1) / per_b;
-      for (int i = rem * per + threadIdx.x; i < min(nwords, (rem + 1) * per); i += kThreads) hist[i] = 0u;
+      const uint32_t hm =
+          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b, s_var) : 0u;
+      score_tile<TT, D, G, 2>(P, io, b, rem / n_rtg, rem % n_rtg, reinterpret_cast<float*>(smem),
+                              part, hm);
+      if (part != PART_EXT) {
+        // Clear this sequence's histograms for the pool stages of this layer.
+        uint32_t* hist = reinterpret_cast<uint32_t*>(a.ws + (size_t)sg.slot * a.w.slot_bytes + a.w.hist) +
+                         (int64_t)b * 2 * P.H * kHistBins;
+        const int nwords = 2 * P.H * kHistBins;
+        const int per = (nwords + per_b - 1) / per_b;
+        for (int i = rem * per + threadIdx.x; i < min(nwords, (rem + 1) * per); i += kThreads) hist[i] = 0u;
+      }
       break;
     }
     case ST_PREP: {
-      const int per_b = P.H * P.n_prep;
+      const int nt = (P.n_prep + kPrepPer - 1) / kPrepPer;
+      const int per_b = P.H * nt;
       const int b = blk / per_b, rem = blk % per_b;
-      task_prep(P, select_io(a, sg.layer, sg.slot), sg.layer, b, rem / P.n_prep, rem % P.n_prep, smem);
+      const int c0 = (rem % nt) * kPrepPer;
+      task_prep(P, select_io(a, sg.layer, sg.slot), sg.layer, b, rem / nt, c0,
+                min(P.n_prep, c0 + kPrepPer), smem);
       break;
     }
-    case ST_POOL: {
-      const int per_b = P.H * P.n_pool;
+    case ST_POOL:
+    case ST_POOLB: {
+      const int nt = (P.n_pool + kPoolPer - 1) / kPoolPer;
+      const int per_b = P.H * nt;
       const int b = blk / per_b, rem = blk % per_b;
-      task_pool(P, select_io(a, sg.layer, sg.slot), b, rem / P.n_pool, rem % P.n_pool, smem);
+      const int c0 = (rem % nt) * kPoolPer;
+      task_pool(P, select_io(a, sg.layer, sg.slot), b, rem / nt, c0, min(P.n_pool, c0 + kPoolPer),
+                smem, true, st == ST_POOL);
+      break;
+    }
+    case ST_POOLX: {
+      const int nt = (P.n_pool + kPoolPer - 1) / kPoolPer;
+      const int per_b = P.delta_eff * nt;
+      const int b = blk / per_b, rem = blk % per_b;
+      const SelectIO io = select_io(a, sg.layer, sg.slot);
+      const int h = nth_bit(htop_mask(P, io.stats, b, s_var), rem / nt);
+      const int c0 = (rem % nt) * kPoolPer;
+      if (h >= 0) task_pool(P, io, b, h, c0, min(P.n_pool, c0 + kPoolPer), smem, false, true);
       break;
     }
     case ST_GATHER: {
@@ -288,14 +359,23 @@ __global__ void coverage_kernel(const uint64_t* bits, int64_t* count, int L, int
 }
 
 int seg_count(const Problem& P, int st) {
+  const bool ext = P.delta_eff > 0;
   switch (st) {
     case ST_SELECT: return P.batch * P.H;
     case ST_COUNT: return P.batch * ((P.words + kCountWords - 1) / kCountWords);
     case ST_PASS1: return P.batch * P.n_kt1 * P.n_rtg;
-    case ST_LSE: return (P.batch * P.HQ * P.Wn + kLseRows - 1) / kLseRows;
+    case ST_P1B: return P.batch * P.n_kt1 * P.n_rtg_base;
+    case ST_P1X: return P.batch * P.n_kt1 * P.n_rtg_x;
+    case ST_LSE:
+    case ST_LSEB: return P.batch * lse_tasks_per_seq(P, st);
+    case ST_LSEX: return P.n_rtg_x ? P.batch * lse_tasks_per_seq(P, st) : 0;
     case ST_PASS2: return P.batch * P.n_kt2 * P.n_rtg;
-    case ST_PREP: return P.batch * P.H * P.n_prep;
-    case ST_POOL: return P.batch * P.H * P.n_pool;
+    case ST_P2B: return P.batch * P.n_kt2 * P.n_rtg_base;
+    case ST_P2X: return P.batch * P.n_kt2 * P.n_rtg_x;
+    case ST_POOL:
+    case ST_POOLB: return P.batch * P.H * ((P.n_pool + kPoolPer - 1) / kPoolPer);
+    case ST_POOLX: return ext ? P.batch * P.delta_eff * ((P.n_pool + kPoolPer - 1) / kPoolPer) : 0;
+    case ST_PREP: return P.batch * P.H * ((P.n_prep + kPrepPer - 1) / kPrepPer);
     case ST_GATHER: return P.batch * P.n_gather;
   }
   return 0;
@@ -398,16 +478,20 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
   a.idx_layer_stride = (int64_t)P.batch * P.H * P.B;
   a.out_layer = 1;
   a.standalone_counts = 0;
-  const int n_launch = P.L + 6;
+  const int n_launch = P.L + kPipeDepth;
   for (int j = 0; j < n_launch; ++j) {
-    set_seg(a, ST_PASS1, j);
-    set_seg(a, ST_LSE, j - 1);
-    set_seg(a, ST_PASS2, j - 2);
-    set_seg(a, ST_POOL, j - 3);
-    set_seg(a, ST_PREP, j - 4);
-    set_seg(a, ST_SELECT, j - 5);
-    set_seg(a, ST_COUNT, j - 5);
-    set_seg(a, ST_GATHER, j - 6);
+    set_seg(a, ST_P1B, j);
+    set_seg(a, ST_LSEB, j - 1);
+    set_seg(a, ST_P2B, j - 2);
+    set_seg(a, ST_POOLB, j - 3);
+    set_seg(a, ST_P1X, j - 4);
+    set_seg(a, ST_LSEX, j - 5);
+    set_seg(a, ST_P2X, j - 6);
+    set_seg(a, ST_POOLX, j - 7);
+    set_seg(a, ST_PREP, j - 8);
+    set_seg(a, ST_SELECT, j - 9);
+    set_seg(a, ST_COUNT, j - 9);
+    set_seg(a, ST_GATHER, j - 10);
     if (ev) (void)hipEventRecord(ev[j], s);
     if ((e = launch(a, w, s)) != hipSuccess) return e;
   }

@@ -271,8 +271,8 @@ struct ScoreTile {
   const Problem& P;
   const ScoreIO& io;
   int b, kt, rtg;
-  int lane, c, n, tpw, h, slot, rt;
-  bool active;
+  int lane, c, n, tpw, h, hs, nh, slot, rt;
+  bool active, idle, exch;
   int r_lo, base_lo, tend, ks, ke, lim_min, nsteps, rr0;
   const char* kbase;
   bool tile_base, tile_mixed, wg_base;
@@ -290,8 +290,9 @@ struct ScoreTile {
   float lsum[NB][4], nlse[NB][4];
   int pos[RB][4];
 
+  // part: which row tiles and heads (PART_EXT: the heads set in hmask).
   __device__ __forceinline__ ScoreTile(const Problem& P_, const ScoreIO& io_, int b_, int kt_,
-                                       int rtg_, float* smem)
+                                       int rtg_, float* smem, Part part, uint32_t hmask)
       : P(P_), io(io_), b(b_), kt(kt_), rtg(rtg_) {
     // wave-uniform by construction; readfirstlane lets the compiler keep the
     // wave's head, tile and buffer resource in scalar registers
@@ -299,11 +300,18 @@ struct ScoreTile {
     lane = threadIdx.x & 63;
     c = lane >> 4;
     n = lane & 15;
-    tpw = 8 / P.H;  // row tiles per work-group
-    h = w % P.H;
-    slot = w / P.H;
-    rt = rtg * tpw + slot;
-    active = slot < tpw && rt < P.n_rt;
+    // wave w: head hs of the pass's nh heads, row tile slot w / nh; with
+    // nh not dividing 8 the last waves are idle
+    nh = part == PART_EXT ? __popc(hmask) : P.H;
+    tpw = 8 / nh;
+    hs = w % nh;
+    slot = w / nh;
+    idle = slot >= tpw;
+    h = part == PART_EXT ? nth_bit(hmask, hs) : hs;
+    const int rt0 = part == PART_EXT ? P.n_rt_base : 0;
+    const int rt_end = part == PART_BASE ? P.n_rt_base : P.n_rt;
+    rt = rt0 + rtg * tpw + slot;
+    active = !idle && rt < rt_end;
     r_lo = P.Wn - (rt + 1) * WR;  // lowest window row of this tile (may be < 0)
     base_lo = P.Wn - P.O;         // first row of the last-O window
 
@@ -356,16 +364,19 @@ struct ScoreTile {
       tile_base = active && r_lo + WR > base_lo;
       tile_mixed = tile_base && r_lo < base_lo;
       // A work-group exchanges importance rows when any of its tiles holds base
-      // rows; the first tile of the group is the newest, so checking it suffices.
-      wg_base = (P.Wn - (rtg * tpw + 1) * WR) + WR > base_lo;
+      // rows; the first tile of the group is the newest, so checking it
+      // suffices.  EXT tiles hold no base rows.
+      wg_base = part != PART_EXT && (P.Wn - (rt0 + rtg * tpw + 1) * WR) + WR > base_lo;
     }
+    exch = PASS == 2 && wg_base && nh > 1;
     rr0 = max(0, base_lo - r_lo);
     // pass-2 LDS per tile slot (after the key rings): two buffers of the
-    // running max over heads [WR][SK + 4] (none for one head), the staged
-    // per-key sums of each head, and the staged importance of the key tile
-    mbuf = smem + key_ring_bytes(ES, D) / 4 + slot * p2_slot_floats(P.H, WR, P.SK, P.tile2);
-    obuf = mbuf + (P.H > 1 ? 2 * WR * (P.SK + 4) : 0);
-    ibuf = obuf + 2 * P.H * P.tile2;
+    // running max over heads [WR][SK + 4] (passes that can exchange), the
+    // staged per-key sums of each head, and the staged importance of the tile
+    const bool layout_x = part != PART_EXT && P.H > 1;
+    mbuf = smem + key_ring_bytes(ES, D) / 4 + slot * p2_slot_floats(nh, WR, P.SK, P.tile2, layout_x);
+    obuf = mbuf + (layout_x ? 2 * WR * (P.SK + 4) : 0);
+    ibuf = obuf + 2 * nh * P.tile2;
   }
 
   // Query fragments.  Padding rows (r < 0) load row 0 and inactive waves
@@ -447,11 +458,11 @@ struct ScoreTile {
       // Stage the per-key sums in LDS; they are written out after the loop so
       // that the loop issues no global stores (exact load counting).
       if (c == 0) {
-        obuf[(h * 2 + 0) * P.tile2 + s * 16 + n] = s_all;
-        obuf[(h * 2 + 1) * P.tile2 + s * 16 + n] = s_base;
+        obuf[(hs * 2 + 0) * P.tile2 + s * 16 + n] = s_all;
+        obuf[(hs * 2 + 1) * P.tile2 + s * 16 + n] = s_base;
       }
       if (tile_base) {
-        if (P.H == 1) {
+        if (nh == 1) {
           // one head: the max over heads is the head itself
           if (c == 0) ibuf[s * 16 + n] = s_base;
         } else {
@@ -479,7 +490,7 @@ struct ScoreTile {
   __device__ __forceinline__ void exchange(int s) {
     lds_barrier();
     const int period = (s * 16) / P.SK;
-    if (tile_base && h == period % P.H) {
+    if (tile_base && hs == period % nh) {
       float* mb = mbuf + (period & 1) * WR * (P.SK + 4);
       for (int kc = lane; kc < P.SK; kc += 64) {
         float v = 0.f;
@@ -519,7 +530,7 @@ struct ScoreTile {
       epilogue<false>(s);
     }
     if constexpr (PASS == 2) {
-      if (wg_base && P.H > 1 && ((s + 1) * 16) % P.SK == 0) exchange(s);
+      if (exch && ((s + 1) * 16) % P.SK == 0) exchange(s);
     }
     // Keep the steps in program order (the next step's waits stay after
     // this step's work).
@@ -538,10 +549,15 @@ struct ScoreTile {
   }
 
   __device__ __forceinline__ void execute() {
+    if (idle) {
+      // no tile: only meet the work-group barrier of the write-out
+      if constexpr (PASS == 2) lds_barrier();
+      return;
+    }
     if constexpr (PASS == 2) {
       // clear both running-max buffers before any head folds rows in
-      if (wg_base && P.H > 1) {
-        for (int i = lane + (h % P.H) * 64; i < 2 * WR * (P.SK + 4); i += 64 * P.H) mbuf[i] = 0.f;
+      if (exch) {
+        for (int i = lane + hs * 64; i < 2 * WR * (P.SK + 4); i += 64 * nh) mbuf[i] = 0.f;
         lds_barrier();
       }
     }
@@ -593,11 +609,11 @@ struct ScoreTile {
         for (int i = lane; i < P.tile2; i += 64) {
           const int t = ks + i;
           if (t < P.Tc) {
-            io.psum_all[o + t] = obuf[(h * 2 + 0) * P.tile2 + i];
-            io.psum_base[o + t] = obuf[(h * 2 + 1) * P.tile2 + i];
+            io.psum_all[o + t] = obuf[(hs * 2 + 0) * P.tile2 + i];
+            io.psum_base[o + t] = obuf[(hs * 2 + 1) * P.tile2 + i];
           }
         }
-        if (tile_base && h == 0) {
+        if (tile_base && hs == 0) {
           for (int i = lane; i < P.tile2; i += 64) {
             const int t = ks + i;
             if (t < P.Tc) io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t] = ibuf[i];
@@ -628,8 +644,8 @@ struct ScoreTile {
 
 template <class TT, int D, int G, int PASS>
 __device__ __forceinline__ void score_tile(const Problem& P, const ScoreIO& io, int b, int kt, int rtg,
-                                           float* smem) {
-  ScoreTile<TT, D, G, PASS> st(P, io, b, kt, rtg, smem);
+                                           float* smem, Part part = PART_ALL, uint32_t hmask = 0) {
+  ScoreTile<TT, D, G, PASS> st(P, io, b, kt, rtg, smem, part, hmask);
   st.execute();
 }
 
@@ -673,23 +689,28 @@ __device__ __noinline__ float2 lse_partial_exact(const Problem P, const char* q,
 
 // Row normalisers: lse2 = log2 of the softmax normaliser of each window row,
 // folded from the pass-1 key-tile partials in tile order.  A task reduces
-// kLseRows rows; 8 threads share a row and merge their partials by shuffles.
+// kLseRows rows of the window rows [r0, r0 + nr) of the heads in hmask; 8
+// threads share a row and merge their partials by shuffles.
 constexpr int kLseRows = 64;
 
 template <class TT, int D, int G>
-__device__ __forceinline__ void task_lse(const Problem& P, const ScoreIO& io, int part) {
-  const int nrows = P.batch * P.HQ * P.Wn;
-  const int row = part * kLseRows + (int)(threadIdx.x >> 3);
+__device__ __forceinline__ void task_lse(const Problem& P, const ScoreIO& io, int b, int task, int r0,
+                                         int nr, uint32_t hmask) {
+  if (nr <= 0) return;
+  const int nrows = P.HQ * nr;
+  // local row = j * nr + rr, window row r = r0 + rr
+  const int lrow = task * kLseRows + (int)(threadIdx.x >> 3);
   const int sub = threadIdx.x & 7;
+  const int rr = lrow % nr, j = lrow / nr;
+  const int r = r0 + rr;
+  const int64_t row = ((int64_t)b * P.HQ + j) * P.Wn + r;
+  const bool live = lrow < nrows && ((hmask >> (j / G)) & 1u);
   float m = -INFINITY, l = 0.f;
-  if (row < nrows) {
-    const float2* pp = io.lse_part + (int64_t)row * P.n_kt1;
+  if (live) {
+    const float2* pp = io.lse_part + row * P.n_kt1;
     for (int t = sub; t < P.n_kt1; t += 8) {
       float2 p = pp[t];
       if (!(p.y < INFINITY)) {
-        // row = (b * HQ + j) * Wn + r
-        const int r = row % P.Wn, bj = row / P.Wn;
-        const int j = bj % P.HQ, b = bj / P.HQ;
         const int64_t qrow = (int64_t)b * io.qs_b + (int64_t)j * io.qs_h + (int64_t)r * io.qs_r;
         const int64_t kb = (int64_t)b * io.ks_b + (int64_t)(j / G) * io.ks_h;
         p = lse_partial_exact<TT, D>(P, io.q, io.k, qrow, kb, io.ks_t, P.T - P.Wn + r, t);
@@ -702,7 +723,7 @@ __device__ __forceinline__ void task_lse(const Problem& P, const ScoreIO& io, in
     const float m2 = __shfl_xor(m, o), l2 = __shfl_xor(l, o);
     lse_merge(m, l, m2, l2);
   }
-  if (row < nrows && sub == 0) io.lse2[row] = m + log2f(l);
+  if (live && sub == 0) io.lse2[row] = m + log2f(l);
 }
 
 }  // namespace kvec

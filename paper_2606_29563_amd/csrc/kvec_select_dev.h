@@ -64,14 +64,16 @@ struct SelectIO {
 };
 
 // ---------------------------------------------------------------------------
-// pool: grid item (b, h, chunk); 512 threads
+// pool: grid item (b, h, chunk); 512 threads.  want_p: pool P (with the sigma
+// sums, the P histogram and, for head 0, I); want_e: pool P over O' (and its
+// histogram).  In the layer pipeline the two run at different times: P first
+// (H_top needs its sigma), P over O' once the extended rows of the H_top
+// heads are scored.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, int b, int h,
-                                          int chunk, char* smem) {
+__device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, int b, int h, int c0,
+                                          int c1, char* smem, bool want_p = true,
+                                          bool want_e = true) {
   const int r = P.pool / 2;
-  const int t0 = chunk * kPoolChunk;
-  const int t1 = min(P.Tc, t0 + kPoolChunk);
-  const int a0 = max(0, t0 - r), a1 = min(P.Tc, t1 + r);
   float* sp = reinterpret_cast<float*>(smem);        // raw P   [a0, a1)
   float* se = sp + (kPoolChunk + 64);                 // raw P'  [a0, a1)
   uint32_t* hp = reinterpret_cast<uint32_t*>(se + (kPoolChunk + 64));
@@ -79,63 +81,76 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
   double* red = reinterpret_cast<double*>(he + kHistBins);
   for (int i = threadIdx.x; i < 2 * kHistBins; i += blockDim.x) hp[i] = 0u;
   const int64_t row = ((int64_t)b * P.H + h) * P.Tc;
-  for (int t = a0 + threadIdx.x; t < a1; t += blockDim.x) {
-    float vp, ve;
-    if (io.psum_all) {
-      float sb = 0.f, sa = 0.f;
-      for (int rt = 0; rt < P.n_rt; ++rt) {
-        const int64_t o = (((int64_t)b * P.n_rt + rt) * P.H + h) * P.Tc + t;
-        if (rt < P.n_rt_base) sb += io.psum_base[o];
-        sa += io.psum_all[o];
+  for (int chunk = c0; chunk < c1; ++chunk) {
+    const int t0 = chunk * kPoolChunk;
+    const int t1 = min(P.Tc, t0 + kPoolChunk);
+    const int a0 = max(0, t0 - r), a1 = min(P.Tc, t1 + r);
+    __syncthreads();  // the previous chunk's window is consumed
+    for (int t = a0 + threadIdx.x; t < a1; t += blockDim.x) {
+      float vp = 0.f, ve = 0.f;
+      if (io.psum_all) {
+        float sb = 0.f, sa = 0.f;
+        for (int rt = 0; rt < P.n_rt; ++rt) {
+          const int64_t o = (((int64_t)b * P.n_rt + rt) * P.H + h) * P.Tc + t;
+          if (want_p && rt < P.n_rt_base) sb += io.psum_base[o];
+          if (want_e) sa += io.psum_all[o];
+        }
+        vp = sb * P.inv_go;
+        ve = sa * P.inv_gwn;
+      } else {
+        if (want_p) vp = io.p_raw[row + t];
+        if (want_e) ve = io.p_ext[row + t];
       }
-      vp = sb * P.inv_go;
-      ve = sa * P.inv_gwn;
-    } else {
-      vp = io.p_raw[row + t];
-      ve = io.p_ext[row + t];
+      sp[t - a0] = vp;
+      se[t - a0] = ve;
     }
-    sp[t - a0] = vp;
-    se[t - a0] = ve;
-  }
-  if (h == 0 && io.psum_all) {
+    if (want_p && h == 0 && io.psum_all) {
+      for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
+        float s = 0.f;
+        for (int rt = 0; rt < P.n_rt_base; ++rt) s += io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t];
+        io.imp[(int64_t)b * P.Tc + t] = s * P.inv_go;
+      }
+    }
+    __syncthreads();
+    double s1 = 0.0, s2 = 0.0;
     for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
-      float s = 0.f;
-      for (int rt = 0; rt < P.n_rt_base; ++rt) s += io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t];
-      io.imp[(int64_t)b * P.Tc + t] = s * P.inv_go;
+      const int u0 = max(0, t - r), u1 = min(P.Tc - 1, t + r);
+      float m = sp[u0 - a0], me = se[u0 - a0];
+      for (int u = u0 + 1; u <= u1; ++u) {
+        m = fmaxf(m, sp[u - a0]);
+        me = fmaxf(me, se[u - a0]);
+      }
+      if (want_p) {
+        io.pooled[row + t] = m;
+        s1 += (double)m;
+        s2 += (double)m * (double)m;
+        atomicAdd(&hp[float_key(m) >> (32 - kHistBits)], 1u);
+      }
+      if (want_e) {
+        io.pooled_ext[row + t] = me;
+        atomicAdd(&he[float_key(me) >> (32 - kHistBits)], 1u);
+      }
+    }
+    if (want_p) {
+      s1 = wave_sum(s1);
+      s2 = wave_sum(s2);
+      const int wid = threadIdx.x >> 6;
+      if ((threadIdx.x & 63) == 0) {
+        red[2 * wid] = s1;
+        red[2 * wid + 1] = s2;
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        double a1 = 0.0, a2 = 0.0;
+        for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
+          a1 += red[2 * i];
+          a2 += red[2 * i + 1];
+        }
+        io.stats[((int64_t)b * P.H + h) * P.n_pool + chunk] = make_double2(a1, a2);
+      }
     }
   }
   __syncthreads();
-  double s1 = 0.0, s2 = 0.0;
-  for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
-    const int u0 = max(0, t - r), u1 = min(P.Tc - 1, t + r);
-    float m = sp[u0 - a0], me = se[u0 - a0];
-    for (int u = u0 + 1; u <= u1; ++u) {
-      m = fmaxf(m, sp[u - a0]);
-      me = fmaxf(me, se[u - a0]);
-    }
-    io.pooled[row + t] = m;
-    io.pooled_ext[row + t] = me;
-    s1 += (double)m;
-    s2 += (double)m * (double)m;
-    atomicAdd(&hp[float_key(m) >> (32 - kHistBits)], 1u);
-    atomicAdd(&he[float_key(me) >> (32 - kHistBits)], 1u);
-  }
-  s1 = wave_sum(s1);
-  s2 = wave_sum(s2);
-  const int wid = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    red[2 * wid] = s1;
-    red[2 * wid + 1] = s2;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double a1 = 0.0, a2 = 0.0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
-      a1 += red[2 * i];
-      a2 += red[2 * i + 1];
-    }
-    io.stats[((int64_t)b * P.H + h) * P.n_pool + chunk] = make_double2(a1, a2);
-  }
   uint32_t* gh = io.hist + ((int64_t)b * 2 * P.H) * kHistBins;
   for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
     if (hp[i]) atomicAdd(&gh[(int64_t)h * kHistBins + i], hp[i]);
@@ -176,40 +191,17 @@ __device__ __forceinline__ int hist_bin_of_rank(const uint32_t* gh, int k, int* 
 // prep: grid item (b, h, chunk); 512 threads
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, int layer, int b,
-                                          int h, int chunk, char* smem) {
-  if (h == 0 && chunk == 0) {
+                                          int h, int c0, int c1, char* smem) {
+  if (h == 0 && c0 == 0) {
     // the selection of this layer ORs its kept tokens into a cleared row
     uint64_t* row = io.bits + ((int64_t)b * P.L + layer) * P.words;
     for (int i = threadIdx.x; i < P.words; i += blockDim.x) row[i] = 0ull;
   }
   double* var = reinterpret_cast<double*>(smem);
-  int* in_top = reinterpret_cast<int*>(var + 8);
-  int* tmp = in_top + 8;
-  if ((int)threadIdx.x < P.H) {
-    const int g = threadIdx.x;
-    double a1 = 0.0, a2 = 0.0;
-    for (int i = 0; i < P.n_pool; ++i) {
-      const double2 v = io.stats[((int64_t)b * P.H + g) * P.n_pool + i];
-      a1 += v.x;
-      a2 += v.y;
-    }
-    const double mean = a1 / P.Tc;
-    var[g] = a2 / P.Tc - mean * mean;
-  }
-  __syncthreads();
-  if ((int)threadIdx.x < P.H) {
-    const int g = threadIdx.x;
-    int rank = 0;
-    for (int o = 0; o < P.H; ++o) rank += (var[o] < var[g]) || (var[o] == var[g] && o < g);
-    in_top[g] = rank < P.delta_eff;
-  }
-  __syncthreads();
-  if (h == 0 && chunk == 0 && threadIdx.x == 0 && io.htop_mask) {
-    uint32_t m = 0;
-    for (int g = 0; g < P.H; ++g) m |= (uint32_t)in_top[g] << g;
-    io.htop_mask[b] = m;
-  }
-  const bool ext = in_top[h] != 0;
+  int* tmp = reinterpret_cast<int*>(var + 8);
+  const uint32_t top = htop_mask(P, io.stats, b, var);
+  if (h == 0 && c0 == 0 && threadIdx.x == 0 && io.htop_mask) io.htop_mask[b] = top;
+  const bool ext = (top >> h) & 1u;
   const float* src = (ext ? io.pooled_ext : io.pooled) + ((int64_t)b * P.H + h) * P.Tc;
   const uint32_t* gh = io.hist + ((int64_t)b * 2 * P.H + (ext ? P.H : 0) + h) * kHistBins;
   const int bin_kp = hist_bin_of_rank(gh, P.Kp, tmp);
@@ -218,33 +210,35 @@ __device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, 
   const float c_edge = bin_m < 0 ? INFINITY : key_float((uint32_t)bin_m << (32 - kHistBits));
   const float thr_u = fminf(c_edge, 1.0f);
   const bool has_preserve = bin_kp >= 0;
-  // Members of this chunk in ascending order: blocked layout, 8 tokens per thread.
-  const int t0 = chunk * kPrepChunk;
-  const int t1 = min(P.Tc, t0 + kPrepChunk);
-  constexpr int per = kPrepChunk / 512;
-  const int lo = min(t1, t0 + (int)threadIdx.x * per), hi = min(t1, lo + per);
   const float* imp = io.imp + (int64_t)b * P.Tc;
-  unsigned flags = 0;
-  int cntm = 0;
-  for (int t = lo; t < hi; ++t) {
-    const float ps = src[t];
-    const float u = __fadd_rn(ps, __fmul_rn(P.lam, imp[t]));
-    const bool m = (has_preserve && float_key(ps) >= kp_edge) || u >= thr_u;
-    flags |= (unsigned)m << (t - lo);
-    cntm += m;
-  }
-  int total;
-  int o = block_excl_scan(cntm, tmp, total);
-  const int64_t base = ((int64_t)b * P.H + h) * P.Tc + t0;
-  for (int t = lo; t < hi; ++t) {
-    if ((flags >> (t - lo)) & 1u) {
-      io.mem_t[base + o] = t;
-      io.mem_ps[base + o] = src[t];
-      io.mem_i[base + o] = imp[t];
-      ++o;
+  for (int chunk = c0; chunk < c1; ++chunk) {
+    // Members of this chunk in ascending order: blocked layout, 2 tokens per thread.
+    const int t0 = chunk * kPrepChunk;
+    const int t1 = min(P.Tc, t0 + kPrepChunk);
+    constexpr int per = kPrepChunk / 512;
+    const int lo = min(t1, t0 + (int)threadIdx.x * per), hi = min(t1, lo + per);
+    unsigned flags = 0;
+    int cntm = 0;
+    for (int t = lo; t < hi; ++t) {
+      const float ps = src[t];
+      const float u = __fadd_rn(ps, __fmul_rn(P.lam, imp[t]));
+      const bool m = (has_preserve && float_key(ps) >= kp_edge) || u >= thr_u;
+      flags |= (unsigned)m << (t - lo);
+      cntm += m;
     }
+    int total;
+    int o = block_excl_scan(cntm, tmp, total);
+    const int64_t base = ((int64_t)b * P.H + h) * P.Tc + t0;
+    for (int t = lo; t < hi; ++t) {
+      if ((flags >> (t - lo)) & 1u) {
+        io.mem_t[base + o] = t;
+        io.mem_ps[base + o] = src[t];
+        io.mem_i[base + o] = imp[t];
+        ++o;
+      }
+    }
+    if (threadIdx.x == 0) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = total;
   }
-  if (threadIdx.x == 0) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = total;
 }
 
 // ---------------------------------------------------------------------------
