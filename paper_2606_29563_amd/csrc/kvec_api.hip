@@ -143,7 +143,7 @@ Workspace make_workspace(const Geometry& g) {
   const size_t p2_ext =
       P.delta_eff > 0 ? (size_t)P.tpw_x * p2_slot_floats(P.delta_eff, P.WR, P.SK, P.tile2, false) : 0;
   const size_t lds_p2 = key_ring_bytes(P.esize, P.D) + (p2_all > p2_ext ? p2_all : p2_ext) * 4;
-  const size_t lds_pool = (size_t)(2 * (kPoolChunk + 64) + 2 * kHistBins) * 4 + 16 * 8;
+  const size_t lds_pool = (size_t)(2 * (kPoolPer * kPoolChunk + 64) + 2 * kHistBins) * 4;
   const size_t lds_prep = 256;
   const size_t lds_sel = 2048 * 4 + 32 * 4 + (size_t)((P.n_prep + 1 + 3) & ~3) * 4 +
                          (size_t)16 * P.mcap;

@@ -15,10 +15,10 @@ constexpr int kRing = kPipeDepth + 1;  // layers in flight in the software pipel
 
 constexpr int kTile1 = 512;       // keys per pass-1 work-group
 constexpr int kTile2Max = 512;    // keys per pass-2 work-group (512 or 256, by LDS)
-constexpr int kPoolChunk = 1024;  // tokens per pool chunk
-constexpr int kPrepChunk = 1024;  // tokens per prep chunk (members are grouped per chunk)
-constexpr int kPoolPer = 4;       // pool chunks per pool work-group
-constexpr int kPrepPer = 8;       // prep chunks per prep work-group
+constexpr int kPoolChunk = 512;   // tokens per pool statistics entry (one wave)
+constexpr int kPrepChunk = 1024;  // tokens per candidate chunk (one wave, 16 per lane)
+constexpr int kPoolPer = 8;       // pool chunks per pool work-group (one per wave)
+constexpr int kPrepPer = 8;       // candidate chunks per prep work-group (one per wave)
 constexpr int kHistBits = 12;     // selection histograms over the top 12 key bits
 constexpr int kHistBins = 1 << kHistBits;
 
@@ -120,41 +120,6 @@ hipError_t run_coverage(const Geometry& g, const uint64_t* bits, int upto, int64
 // Device helpers
 // ---------------------------------------------------------------------------
 
-// H_top (Sec. 4.1): bit h set for the delta_eff heads of sequence b with the
-// lowest variance of pooled P (ties: lower head), from the per-chunk float64
-// sums of the pool stage.  Every caller computes it the same way, so the
-// score passes of the extended window and the selection agree.  Work-group
-// cooperative (barriers); `vars` holds 8 doubles of shared memory.
-__device__ __forceinline__ uint32_t htop_mask(const Problem& P, const double2* stats, int b,
-                                              double* vars) {
-  if ((int)threadIdx.x < P.H) {
-    const int g = threadIdx.x;
-    double a1 = 0.0, a2 = 0.0;
-    for (int i = 0; i < P.n_pool; ++i) {
-      const double2 v = stats[((int64_t)b * P.H + g) * P.n_pool + i];
-      a1 += v.x;
-      a2 += v.y;
-    }
-    const double mean = a1 / P.Tc;
-    vars[g] = a2 / P.Tc - mean * mean;
-  }
-  __syncthreads();
-  uint32_t m = 0;
-  for (int g = 0; g < P.H; ++g) {
-    int rank = 0;
-    for (int o = 0; o < P.H; ++o) rank += (vars[o] < vars[g]) || (vars[o] == vars[g] && o < g);
-    m |= (uint32_t)(rank < P.delta_eff) << g;
-  }
-  __syncthreads();
-  return m;
-}
-
-// Index of the k-th set bit of m, or -1 when m has at most k set bits.
-__device__ __forceinline__ int nth_bit(uint32_t m, int k) {
-  for (int i = 0; i < k; ++i) m &= m - 1u;
-  return __ffs(m) - 1;
-}
-
 // Order-preserving map of an IEEE float to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t float_key(float f) {
   const uint32_t u = __float_as_uint(f);
@@ -198,6 +163,46 @@ __device__ __forceinline__ int block_excl_scan(int v, int* tmp, int& total) {
   total = tmp[16];
   __syncthreads();
   return r;
+}
+
+// H_top (Sec. 4.1): bit h set for the delta_eff heads of sequence b with the
+// lowest variance of pooled P (ties: lower head), from the per-chunk float64
+// sums of the pool stage.  Every caller computes it the same way, so the
+// score passes of the extended window and the selection agree.  Work-group
+// cooperative (barriers); `vars` holds 8 doubles of shared memory.
+__device__ __forceinline__ uint32_t htop_mask(const Problem& P, const double2* stats, int b,
+                                              double* vars) {
+  // wave g sums head g's per-chunk partials (lane-strided, then a wave sum)
+  const int g = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (g < P.H) {
+    double a1 = 0.0, a2 = 0.0;
+    for (int i = lane; i < P.n_pool; i += 64) {
+      const double2 v = stats[((int64_t)b * P.H + g) * P.n_pool + i];
+      a1 += v.x;
+      a2 += v.y;
+    }
+    a1 = wave_sum(a1);
+    a2 = wave_sum(a2);
+    if (lane == 0) {
+      const double mean = a1 / P.Tc;
+      vars[g] = a2 / P.Tc - mean * mean;
+    }
+  }
+  __syncthreads();
+  uint32_t m = 0;
+  for (int h = 0; h < P.H; ++h) {
+    int rank = 0;
+    for (int o = 0; o < P.H; ++o) rank += (vars[o] < vars[h]) || (vars[o] == vars[h] && o < h);
+    m |= (uint32_t)(rank < P.delta_eff) << h;
+  }
+  __syncthreads();
+  return m;
+}
+
+// Index of the k-th set bit of m, or -1 when m has at most k set bits.
+__device__ __forceinline__ int nth_bit(uint32_t m, int k) {
+  for (int i = 0; i < k; ++i) m &= m - 1u;
+  return __ffs(m) - 1;
 }
 
 }  // namespace kvec

@@ -73,47 +73,102 @@ struct SelectIO {
 __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, int b, int h, int c0,
                                           int c1, char* smem, bool want_p = true,
                                           bool want_e = true) {
+  // Wave w pools chunk c0 + w (kPoolChunk tokens, kPoolChunk / 64 per lane,
+  // lane-strided so stores coalesce) out of one LDS window holding the whole
+  // span with its halo.
   const int r = P.pool / 2;
+  const int t0 = c0 * kPoolChunk;
+  const int t1 = min(P.Tc, c1 * kPoolChunk);
+  const int a0 = max(0, t0 - r), a1 = min(P.Tc, t1 + r);
   float* sp = reinterpret_cast<float*>(smem);        // raw P   [a0, a1)
-  float* se = sp + (kPoolChunk + 64);                 // raw P'  [a0, a1)
-  uint32_t* hp = reinterpret_cast<uint32_t*>(se + (kPoolChunk + 64));
+  float* se = sp + (kPoolPer * kPoolChunk + 64);      // raw P'  [a0, a1)
+  uint32_t* hp = reinterpret_cast<uint32_t*>(se + (kPoolPer * kPoolChunk + 64));
   uint32_t* he = hp + kHistBins;
-  double* red = reinterpret_cast<double*>(he + kHistBins);
   for (int i = threadIdx.x; i < 2 * kHistBins; i += blockDim.x) hp[i] = 0u;
   const int64_t row = ((int64_t)b * P.H + h) * P.Tc;
-  for (int chunk = c0; chunk < c1; ++chunk) {
-    const int t0 = chunk * kPoolChunk;
-    const int t1 = min(P.Tc, t0 + kPoolChunk);
-    const int a0 = max(0, t0 - r), a1 = min(P.Tc, t1 + r);
-    __syncthreads();  // the previous chunk's window is consumed
-    for (int t = a0 + threadIdx.x; t < a1; t += blockDim.x) {
-      float vp = 0.f, ve = 0.f;
-      if (io.psum_all) {
-        float sb = 0.f, sa = 0.f;
-        for (int rt = 0; rt < P.n_rt; ++rt) {
-          const int64_t o = (((int64_t)b * P.n_rt + rt) * P.H + h) * P.Tc + t;
-          if (want_p && rt < P.n_rt_base) sb += io.psum_base[o];
-          if (want_e) sa += io.psum_all[o];
+  // The window is at most kPoolPer * kPoolChunk + 62 tokens: kSpan loads per
+  // thread, unrolled so that every load of the thread is in flight at once.
+  constexpr int kSpan = (kPoolPer * kPoolChunk + 64) / kThreads + 1;
+  float vp[kSpan], ve[kSpan];
+#pragma unroll
+  for (int k = 0; k < kSpan; ++k) {
+    vp[k] = 0.f;
+    ve[k] = 0.f;
+  }
+  if (io.psum_all) {
+    // rows summed in row-tile order, as in the stand-alone finaliser; four
+    // row tiles' loads are issued before any of them is used
+    const int nrt = want_e ? P.n_rt : P.n_rt_base;
+    for (int rt0 = 0; rt0 < nrt; rt0 += 4) {
+      float lp[4][kSpan], le[4][kSpan];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rt = rt0 + q;
+        const bool add_p = want_p && rt < P.n_rt_base;
+        const int64_t o = (((int64_t)b * P.n_rt + rt) * P.H + h) * P.Tc;
+#pragma unroll
+        for (int k = 0; k < kSpan; ++k) {
+          const int t = a0 + (int)threadIdx.x + k * kThreads;
+          lp[q][k] = add_p && t < a1 ? io.psum_base[o + t] : 0.f;
+          le[q][k] = want_e && rt < nrt && t < a1 ? io.psum_all[o + t] : 0.f;
         }
-        vp = sb * P.inv_go;
-        ve = sa * P.inv_gwn;
-      } else {
-        if (want_p) vp = io.p_raw[row + t];
-        if (want_e) ve = io.p_ext[row + t];
       }
-      sp[t - a0] = vp;
-      se[t - a0] = ve;
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int k = 0; k < kSpan; ++k) {
+          vp[k] += lp[q][k];
+          ve[k] += le[q][k];
+        }
     }
-    if (want_p && h == 0 && io.psum_all) {
-      for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
-        float s = 0.f;
-        for (int rt = 0; rt < P.n_rt_base; ++rt) s += io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t];
-        io.imp[(int64_t)b * P.Tc + t] = s * P.inv_go;
+#pragma unroll
+    for (int k = 0; k < kSpan; ++k) {
+      vp[k] *= P.inv_go;
+      ve[k] *= P.inv_gwn;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < kSpan; ++k) {
+      const int t = a0 + (int)threadIdx.x + k * kThreads;
+      if (t < a1) {
+        if (want_p) vp[k] = io.p_raw[row + t];
+        if (want_e) ve[k] = io.p_ext[row + t];
       }
     }
-    __syncthreads();
+  }
+#pragma unroll
+  for (int k = 0; k < kSpan; ++k) {
+    const int t = a0 + (int)threadIdx.x + k * kThreads;
+    if (t < a1) {
+      sp[t - a0] = vp[k];
+      se[t - a0] = ve[k];
+    }
+  }
+  if (want_p && h == 0 && io.psum_all) {
+    constexpr int kOwn = kPoolPer * kPoolChunk / kThreads;
+    float si[kOwn];
+#pragma unroll
+    for (int k = 0; k < kOwn; ++k) si[k] = 0.f;
+    for (int rt = 0; rt < P.n_rt_base; ++rt) {
+#pragma unroll
+      for (int k = 0; k < kOwn; ++k) {
+        const int t = t0 + (int)threadIdx.x + k * kThreads;
+        if (t < t1) si[k] += io.ipart[((int64_t)b * P.n_rt + rt) * P.Tc + t];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kOwn; ++k) {
+      const int t = t0 + (int)threadIdx.x + k * kThreads;
+      if (t < t1) io.imp[(int64_t)b * P.Tc + t] = si[k] * P.inv_go;
+    }
+  }
+  __syncthreads();
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int chunk = c0 + w;
+  if (chunk < c1) {
+    const int ct0 = chunk * kPoolChunk, ct1 = min(P.Tc, ct0 + kPoolChunk);
     double s1 = 0.0, s2 = 0.0;
-    for (int t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
+    for (int t = ct0 + lane; t < ct1; t += 64) {
       const int u0 = max(0, t - r), u1 = min(P.Tc - 1, t + r);
       float m = sp[u0 - a0], me = se[u0 - a0];
       for (int u = u0 + 1; u <= u1; ++u) {
@@ -134,20 +189,7 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
     if (want_p) {
       s1 = wave_sum(s1);
       s2 = wave_sum(s2);
-      const int wid = threadIdx.x >> 6;
-      if ((threadIdx.x & 63) == 0) {
-        red[2 * wid] = s1;
-        red[2 * wid + 1] = s2;
-      }
-      __syncthreads();
-      if (threadIdx.x == 0) {
-        double a1 = 0.0, a2 = 0.0;
-        for (int i = 0; i < (int)(blockDim.x >> 6); ++i) {
-          a1 += red[2 * i];
-          a2 += red[2 * i + 1];
-        }
-        io.stats[((int64_t)b * P.H + h) * P.n_pool + chunk] = make_double2(a1, a2);
-      }
+      if (lane == 0) io.stats[((int64_t)b * P.H + h) * P.n_pool + chunk] = make_double2(s1, s2);
     }
   }
   __syncthreads();
@@ -211,33 +253,45 @@ __device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, 
   const float thr_u = fminf(c_edge, 1.0f);
   const bool has_preserve = bin_kp >= 0;
   const float* imp = io.imp + (int64_t)b * P.Tc;
-  for (int chunk = c0; chunk < c1; ++chunk) {
-    // Members of this chunk in ascending order: blocked layout, 2 tokens per thread.
+  // Wave w extracts chunk c0 + w: lane l scans tokens [16 l, 16 l + 16) of
+  // the chunk, a wave scan gives the members' offsets in ascending order.
+  static_assert(kPrepChunk == 64 * 16, "one chunk per wave, 16 tokens per lane");
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int chunk = c0 + w;
+  if (chunk < c1) {
     const int t0 = chunk * kPrepChunk;
     const int t1 = min(P.Tc, t0 + kPrepChunk);
-    constexpr int per = kPrepChunk / 512;
-    const int lo = min(t1, t0 + (int)threadIdx.x * per), hi = min(t1, lo + per);
+    const int lo = t0 + lane * 16;
+    // all 32 loads of the lane in flight at once
+    float ps[16], im[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int t = min(lo + k, t1 - 1);
+      ps[k] = src[t];
+      im[k] = imp[t];
+    }
     unsigned flags = 0;
     int cntm = 0;
-    for (int t = lo; t < hi; ++t) {
-      const float ps = src[t];
-      const float u = __fadd_rn(ps, __fmul_rn(P.lam, imp[t]));
-      const bool m = (has_preserve && float_key(ps) >= kp_edge) || u >= thr_u;
-      flags |= (unsigned)m << (t - lo);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float u = __fadd_rn(ps[k], __fmul_rn(P.lam, im[k]));
+      const bool m = lo + k < t1 && ((has_preserve && float_key(ps[k]) >= kp_edge) || u >= thr_u);
+      flags |= (unsigned)m << k;
       cntm += m;
     }
-    int total;
-    int o = block_excl_scan(cntm, tmp, total);
+    const int incl = wave_incl_scan(cntm);
+    int o = incl - cntm;
     const int64_t base = ((int64_t)b * P.H + h) * P.Tc + t0;
-    for (int t = lo; t < hi; ++t) {
-      if ((flags >> (t - lo)) & 1u) {
-        io.mem_t[base + o] = t;
-        io.mem_ps[base + o] = src[t];
-        io.mem_i[base + o] = imp[t];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      if ((flags >> k) & 1u) {
+        io.mem_t[base + o] = lo + k;
+        io.mem_ps[base + o] = ps[k];
+        io.mem_i[base + o] = im[k];
         ++o;
       }
     }
-    if (threadIdx.x == 0) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = total;
+    if (lane == 63) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = incl;
   }
 }
 
