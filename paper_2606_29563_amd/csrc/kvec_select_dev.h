@@ -200,35 +200,6 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
   }
 }
 
-// Bin holding the k-th largest key (1 <= k <= total) of a histogram, by a
-// block-wide descending prefix sum.  Returns -1 for k <= 0.
-__device__ __forceinline__ int hist_bin_of_rank(const uint32_t* gh, int k, int* tmp) {
-  if (k <= 0) return -1;
-  constexpr int per = kHistBins / 512;
-  const int tid = threadIdx.x;  // owns bins [kHistBins-1-tid*per, ... descending)
-  int cnt[per], s = 0;
-#pragma unroll
-  for (int e = 0; e < per; ++e) {
-    cnt[e] = (int)gh[kHistBins - 1 - (tid * per + e)];
-    s += cnt[e];
-  }
-  int total;
-  const int before = block_excl_scan(s, tmp, total);
-  if (before < k && k <= before + s) {
-    int run = before, found = -1;
-#pragma unroll
-    for (int e = 0; e < per; ++e) {
-      if (found < 0 && run + cnt[e] >= k) found = e;
-      run += cnt[e];
-    }
-    tmp[20] = kHistBins - 1 - (tid * per + found);
-  }
-  __syncthreads();
-  const int bin = tmp[20];
-  __syncthreads();
-  return bin;
-}
-
 // ---------------------------------------------------------------------------
 // prep: grid item (b, h, chunk); 512 threads
 // ---------------------------------------------------------------------------
@@ -241,57 +212,92 @@ __device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, 
   }
   double* var = reinterpret_cast<double*>(smem);
   int* tmp = reinterpret_cast<int*>(var + 8);
+  // Every load is issued before H_top is known (one memory round trip):
+  // both histograms of head h, and both pooled scores and I of this wave's
+  // chunk (wave w extracts chunk c0 + w; round k covers tokens
+  // [64 k, 64 k + 64) of the chunk, one per lane, so loads coalesce).
+  constexpr int per = kHistBins / 512;
+  const int tid = threadIdx.x;  // owns bins kHistBins-1-tid*per ... (descending)
+  const uint32_t* ghp = io.hist + ((int64_t)b * 2 * P.H + h) * kHistBins;
+  const uint32_t* ghe = ghp + (int64_t)P.H * kHistBins;
+  int cp[per], ce[per];
+#pragma unroll
+  for (int e = 0; e < per; ++e) {
+    cp[e] = (int)ghp[kHistBins - 1 - (tid * per + e)];
+    ce[e] = (int)ghe[kHistBins - 1 - (tid * per + e)];
+  }
+  static_assert(kPrepChunk == 64 * 16, "one chunk per wave, 16 rounds of 64 tokens");
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int chunk = c0 + w;
+  const bool has_chunk = chunk < c1;
+  const int t0 = chunk * kPrepChunk;
+  const int t1 = min(P.Tc, t0 + kPrepChunk);
+  const int64_t hrow = ((int64_t)b * P.H + h) * P.Tc;
+  const float* imp = io.imp + (int64_t)b * P.Tc;
+  float pp[16], pe[16], im[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const int t = has_chunk ? min(t0 + k * 64 + lane, t1 - 1) : 0;
+    pp[k] = io.pooled[hrow + t];
+    pe[k] = io.pooled_ext[hrow + t];
+    im[k] = imp[t];
+  }
   const uint32_t top = htop_mask(P, io.stats, b, var);
   if (h == 0 && c0 == 0 && threadIdx.x == 0 && io.htop_mask) io.htop_mask[b] = top;
   const bool ext = (top >> h) & 1u;
-  const float* src = (ext ? io.pooled_ext : io.pooled) + ((int64_t)b * P.H + h) * P.Tc;
-  const uint32_t* gh = io.hist + ((int64_t)b * 2 * P.H + (ext ? P.H : 0) + h) * kHistBins;
-  const int bin_kp = hist_bin_of_rank(gh, P.Kp, tmp);
-  const int bin_m = hist_bin_of_rank(gh, P.M, tmp);
+  // Bins holding the Kp-th and the M-th largest key, from one descending
+  // prefix sum of the selected histogram.
+  int s = 0;
+#pragma unroll
+  for (int e = 0; e < per; ++e) s += ext ? ce[e] : cp[e];
+  if (threadIdx.x == 0) {
+    tmp[20] = -1;
+    tmp[21] = -1;
+  }
+  int total;
+  const int before = block_excl_scan(s, tmp, total);
+  const int ranks[2] = {P.Kp, P.M};
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int k = ranks[q];
+    if (k > 0 && before < k && k <= before + s) {
+      int run = before, found = -1;
+#pragma unroll
+      for (int e = 0; e < per; ++e) {
+        if (found < 0 && run + (ext ? ce[e] : cp[e]) >= k) found = e;
+        run += ext ? ce[e] : cp[e];
+      }
+      tmp[20 + q] = kHistBins - 1 - (tid * per + found);
+    }
+  }
+  __syncthreads();
+  const int bin_kp = tmp[20], bin_m = tmp[21];
   const uint32_t kp_edge = bin_kp < 0 ? 0xffffffffu : (uint32_t)bin_kp << (32 - kHistBits);
   const float c_edge = bin_m < 0 ? INFINITY : key_float((uint32_t)bin_m << (32 - kHistBits));
   const float thr_u = fminf(c_edge, 1.0f);
   const bool has_preserve = bin_kp >= 0;
-  const float* imp = io.imp + (int64_t)b * P.Tc;
-  // Wave w extracts chunk c0 + w: lane l scans tokens [16 l, 16 l + 16) of
-  // the chunk, a wave scan gives the members' offsets in ascending order.
-  static_assert(kPrepChunk == 64 * 16, "one chunk per wave, 16 tokens per lane");
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int chunk = c0 + w;
-  if (chunk < c1) {
-    const int t0 = chunk * kPrepChunk;
-    const int t1 = min(P.Tc, t0 + kPrepChunk);
-    const int lo = t0 + lane * 16;
-    // all 32 loads of the lane in flight at once
-    float ps[16], im[16];
+  if (has_chunk) {
+    // members of the chunk in ascending order: round by round, each member's
+    // place is the members before it (earlier rounds, then lower lanes)
+    const int64_t base = hrow + t0;
+    int off = 0;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
-      const int t = min(lo + k, t1 - 1);
-      ps[k] = src[t];
-      im[k] = imp[t];
-    }
-    unsigned flags = 0;
-    int cntm = 0;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const float u = __fadd_rn(ps[k], __fmul_rn(P.lam, im[k]));
-      const bool m = lo + k < t1 && ((has_preserve && float_key(ps[k]) >= kp_edge) || u >= thr_u);
-      flags |= (unsigned)m << k;
-      cntm += m;
-    }
-    const int incl = wave_incl_scan(cntm);
-    int o = incl - cntm;
-    const int64_t base = ((int64_t)b * P.H + h) * P.Tc + t0;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      if ((flags >> k) & 1u) {
-        io.mem_t[base + o] = lo + k;
-        io.mem_ps[base + o] = ps[k];
-        io.mem_i[base + o] = im[k];
-        ++o;
+      const int t = t0 + k * 64 + lane;
+      const float ps = ext ? pe[k] : pp[k];
+      const float u = __fadd_rn(ps, __fmul_rn(P.lam, im[k]));
+      const bool m = t < t1 && ((has_preserve && float_key(ps) >= kp_edge) || u >= thr_u);
+      const uint64_t mask = __ballot(m);
+      const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+      if (m) {
+        io.mem_t[base + off + before] = t;
+        io.mem_ps[base + off + before] = ps;
+        io.mem_i[base + off + before] = im[k];
       }
+      off += __popcll(mask);
     }
-    if (lane == 63) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = incl;
+    if (lane == 0) io.mem_n[((int64_t)b * P.H + h) * P.n_prep + chunk] = off;
   }
 }
 
