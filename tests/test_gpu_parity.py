@@ -254,3 +254,52 @@ def test_layer_calls_match_model_step(gpu_lib):
     assert torch.equal(bits_m, bits_l)
     assert torch.equal(ko_m.view(torch.int16), ko_l.view(torch.int16))
     assert torch.equal(vo_m.view(torch.int16), vo_l.view(torch.int16))
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, run exactly as the benchmark runs them (kvec_evict_model
+# over every layer with the library-sized workspace); the oracle checks every
+# layer at 4k and sampled layers of the larger shapes, teacher-forced on the
+# device's own bitmaps of the earlier layers.
+# ---------------------------------------------------------------------------
+
+def test_full_llama8b_4k_every_layer(gpu_lib):
+    _e2e(gpu_lib, synth.workload(1))
+
+
+def test_full_llama8b_32k_sampled_layers(gpu_lib):
+    _e2e(gpu_lib, synth.workload(2), check_layers=[0, 1, 15, 31])
+
+
+def test_full_llama8b_16k_batch8_sampled_layers(gpu_lib):
+    _e2e(gpu_lib, synth.workload(3), check_layers=[0, 31])
+
+
+def test_full_llama8b_128k_sampled_layers(gpu_lib):
+    _e2e(gpu_lib, synth.workload(4), check_layers=[0, 31])
+
+
+@pytest.mark.parametrize("wi", [2, 3, 4], ids=["32k", "16k-b8", "128k"])
+def test_full_size_scores(gpu_lib, wi):
+    """kvec_score on one layer of a full-size shape against the oracle scores."""
+    import torch
+    kv = gpu_lib
+    w = synth.workload(wi)
+    w1 = w.with_(batch=1)
+    cfg = kv.Config.from_workload(w1)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    layer = w.n_layers - 1
+    qa, ka, _ = layer_inputs(w1, layer, 0)
+    q = to_device(qa, w1)[None]
+    k = to_device(ka, w1)[None]
+    Tc = w1.candidates
+    p = torch.empty((1, w1.n_kv_heads, Tc), dtype=torch.float32, device="cuda")
+    pe = torch.empty_like(p)
+    imp = torch.empty((1, Tc), dtype=torch.float32, device="cuda")
+    kv.kvec_score(cfg, q, k, p, pe, imp, ws)
+    torch.cuda.synchronize()
+    rp, rpe, rimp = oracle_scores(w1, layer, 0, qa, ka)
+    e = (rel_err(p[0].cpu().numpy(), rp), rel_err(pe[0].cpu().numpy(), rpe),
+         rel_err(imp[0].cpu().numpy(), rimp))
+    _say(f"[score] {w.name} layer {layer}: rel err P {e[0]:.2e} P' {e[1]:.2e} I {e[2]:.2e}")
+    assert max(e) <= SCORE_RTOL, e
