@@ -474,8 +474,9 @@ struct ScoreTile {
           for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
+              // rows before rr0 (not in the last-O window) fold in a zero
               const int rr = rb * 16 + 4 * c + i;
-              if (rr >= rr0) lds_max_u32(mb + rr * (P.SK + 4) + kk, __float_as_uint(gs[rb][i]));
+              lds_max_u32(mb + rr * (P.SK + 4) + kk, rr >= rr0 ? __float_as_uint(gs[rb][i]) : 0u);
             }
         }
       }
@@ -483,23 +484,31 @@ struct ScoreTile {
   }
 
   // End of an exchange period of SK keys (step s is its last): once every
-  // head of the slot has folded its rows in, one wave of the slot (rotating)
-  // sums the maxima over the rows into the importance of those keys and
-  // clears the buffer, which is written again two periods later, after the
-  // next period's barrier.
+  // head of the slot has folded its rows in, the slot's waves share the keys
+  // of the period: lane (kc, rg) of a wave sums rows rg, rg + 4, ... of key
+  // kc, the four row groups are added across lanes, and the buffer is
+  // cleared for its reuse two periods later (after the next barrier).
   __device__ __forceinline__ void exchange(int s) {
     lds_barrier();
+    if (!tile_base) return;
     const int period = (s * 16) / P.SK;
-    if (tile_base && hs == period % nh) {
-      float* mb = mbuf + (period & 1) * WR * (P.SK + 4);
-      for (int kc = lane; kc < P.SK; kc += 64) {
-        float v = 0.f;
-        for (int rr = 0; rr < WR; ++rr) {  // rows before rr0 stay zero
+    float* mb = mbuf + (period & 1) * WR * (P.SK + 4);
+    const int kpw = (P.SK + nh - 1) / nh;
+    const int kb0 = hs * kpw, kb1 = min(P.SK, kb0 + kpw);
+    const int rg = lane >> 4;
+    for (int k0 = kb0; k0 < kb1; k0 += 16) {
+      const int kc = k0 + (lane & 15);
+      const bool ok = kc < kb1;
+      float v = 0.f;
+      if (ok) {
+#pragma unroll
+        for (int rr = rg; rr < WR; rr += 4) {
           v += mb[rr * (P.SK + 4) + kc];
           mb[rr * (P.SK + 4) + kc] = 0.f;
         }
-        ibuf[period * P.SK + kc] = v;
       }
+      v = col_sum4(v);
+      if (ok && rg == 0) ibuf[period * P.SK + kc] = v;
     }
   }
 
