@@ -122,6 +122,16 @@ __device__ __forceinline__ f32x4 mma(const Frag<F32, D>& a, const Frag<F32, D>& 
   return acc;
 }
 
+// One k-step (32 bf16 or 4 fp32 elements of the head dimension) of a block.
+template <int D>
+__device__ __forceinline__ f32x4 mma1(const Frag<BF16, D>& a, const Frag<BF16, D>& b, f32x4 acc, int j) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v[j], b.v[j], acc, 0, 0, 0);
+}
+template <int D>
+__device__ __forceinline__ f32x4 mma1(const Frag<F32, D>& a, const Frag<F32, D>& b, f32x4 acc, int j) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[j], b.v[j], acc, 0, 0, 0);
+}
+
 template <class TT>
 constexpr int elem_bytes() { return __is_same(TT, BF16) ? 2 : 4; }
 
@@ -410,8 +420,14 @@ struct ScoreTile {
 
   template <int F>
   __device__ __forceinline__ void mma_frag() {
+    // k-step-major: consecutive MFMAs write different blocks, so each block's
+    // accumulation chain has NB - 1 independent products between its links
 #pragma unroll
-    for (int bk = 0; bk < NB; ++bk) acc[bk] = mma<D>(qf[bk], kf[F], f32x4{0.f, 0.f, 0.f, 0.f});
+    for (int bk = 0; bk < NB; ++bk) acc[bk] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < Frag<TT, D>::KS; ++j)
+#pragma unroll
+      for (int bk = 0; bk < NB; ++bk) acc[bk] = mma1<D>(qf[bk], kf[F], acc[bk], j);
   }
 
   template <bool MASKED>
