@@ -60,6 +60,7 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   x.WR = 16 * row_blocks_per_tile(G);
   x.n_rt = (x.Wn + x.WR - 1) / x.WR;
   x.n_rt_base = (x.O + x.WR - 1) / x.WR;
+  x.nsum = x.O % x.WR == 0 ? 1 : 2;
   const int tpw = 8 / H;
   x.n_rtg = (x.n_rt + tpw - 1) / tpw;
   x.n_kt1 = (x.T + kTile1 - 1) / kTile1;
@@ -75,14 +76,15 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   x.tpw_x = x.delta_eff > 0 ? 8 / x.delta_eff : 0;
   x.n_rtg_x = x.delta_eff > 0 && n_rt_ext > 0 ? (n_rt_ext + x.tpw_x - 1) / x.tpw_x : 0;
   auto lds_p2 = [&](int sk, int tile) {
-    const size_t all = (size_t)tpw * p2_slot_floats(H, x.WR, sk, tile, H > 1);
-    const size_t ext = x.delta_eff > 0 ? (size_t)x.tpw_x * p2_slot_floats(x.delta_eff, x.WR, sk, tile, false) : 0;
+    const size_t all = (size_t)tpw * p2_slot_floats(H, x.WR, sk, tile, H > 1, x.nsum);
+    const size_t ext =
+        x.delta_eff > 0 ? (size_t)x.tpw_x * p2_slot_floats(x.delta_eff, x.WR, sk, tile, false, x.nsum) : 0;
     return ring + (all > ext ? all : ext) * 4;
   };
   const size_t lds_cap = kLdsMax - kLdsStatic;
   x.tile2 = 0;
   for (int tile = kTile2Max; tile >= kTile2Max / 2 && !x.tile2; tile /= 2)
-    for (int sk = 128; sk >= (tile == kTile2Max ? 32 : 16); sk /= 2)
+    for (int sk = tile; sk >= (tile == kTile2Max ? 32 : 16); sk = sk == tile ? 128 : sk / 2)
       if (lds_p2(sk, tile) <= lds_cap) {
         x.tile2 = tile;
         x.SK = sk;
@@ -139,9 +141,9 @@ Workspace make_workspace(const Geometry& g) {
   w.total = off;
   // dynamic LDS: the largest task
   const int tpw = 8 / P.H;
-  const size_t p2_all = (size_t)tpw * p2_slot_floats(P.H, P.WR, P.SK, P.tile2, P.H > 1);
+  const size_t p2_all = (size_t)tpw * p2_slot_floats(P.H, P.WR, P.SK, P.tile2, P.H > 1, P.nsum);
   const size_t p2_ext =
-      P.delta_eff > 0 ? (size_t)P.tpw_x * p2_slot_floats(P.delta_eff, P.WR, P.SK, P.tile2, false) : 0;
+      P.delta_eff > 0 ? (size_t)P.tpw_x * p2_slot_floats(P.delta_eff, P.WR, P.SK, P.tile2, false, P.nsum) : 0;
   const size_t lds_p2 = key_ring_bytes(P.esize, P.D) + (p2_all > p2_ext ? p2_all : p2_ext) * 4;
   const size_t lds_pool = (size_t)(2 * (kPoolPer * kPoolChunk + 64) + 2 * kHistBins) * 4;
   const size_t lds_prep = 256;

@@ -43,11 +43,15 @@ constexpr int key_ring_slots(int esize, int D) {
 constexpr size_t key_ring_bytes(int esize, int D) {
   return (size_t)(kThreads / 64) * key_ring_slots(esize, D) * 16 * D * esize;
 }
-// Pass-2 LDS floats per row-tile slot of nh heads: two running-max buffers
-// [WR][SK + 4] when the slot exchanges the importance over heads, per-key
-// sums of each head (base and all rows) and the importance of the key tile.
-__host__ __device__ constexpr int p2_slot_floats(int nh, int WR, int SK, int tile2, bool exchange) {
-  return (exchange ? 2 * WR * (SK + 4) : 0) + 2 * nh * tile2 + tile2;
+// Pass-2 LDS floats per row-tile slot of nh heads: the running-max buffers
+// [WR][SK + 4] when the slot exchanges the importance over heads (one when
+// the exchange period is the whole key tile, else two, used in turn), per-key
+// sums of each head (nsum of them: all rows, and the last-O rows when a row
+// tile can hold both kinds) and the importance of the key tile.
+__host__ __device__ constexpr int exchange_buffers(int SK, int tile2) { return SK >= tile2 ? 1 : 2; }
+__host__ __device__ constexpr int p2_slot_floats(int nh, int WR, int SK, int tile2, bool exchange,
+                                                 int nsum) {
+  return (exchange ? exchange_buffers(SK, tile2) * WR * (SK + 4) : 0) + nsum * nh * tile2 + tile2;
 }
 
 // Which window rows and heads a score pass covers.  ALL: every row tile and
@@ -61,6 +65,8 @@ struct Problem {
   int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;
   float lam, sc, inv_go, inv_gwn;
   int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK, tile2;
+  int nsum;        // pass-2 per-key sums per head: 1 when O is a multiple of WR (no row
+                   // tile holds both last-O and earlier rows), else 2
   int n_rtg_base;  // work-groups per key tile of a BASE pass (8/H row tiles each)
   int tpw_x;       // row tiles per work-group of an EXT pass (8 / delta_eff)
   int n_rtg_x;     // work-groups per key tile of an EXT pass (0: no EXT pass)

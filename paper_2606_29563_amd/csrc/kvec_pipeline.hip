@@ -131,32 +131,46 @@ __device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int 
 }
 
 // Cache store (Sec. 4.1): out[b][h][i] = K[b][h][idx[b][h][i]] (and V),
-// one 16-byte chunk per thread and iteration; idx outside [0, T) -> zeros.
+// one 16-byte chunk per thread and round, 4 rounds per work-group; idx
+// outside [0, T) -> zeros.  All index loads are issued first, then all row
+// loads, then the stores (one memory round trip each).
 __device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b, int part) {
+  constexpr int kRounds = 4;
   const Problem& P = a.P;
   const int cpr = P.D * P.esize / 16;
   const int64_t total = (int64_t)P.H * P.B * cpr;
   const int32_t* idx = a.idx + (int64_t)layer * a.idx_layer_stride + (int64_t)b * P.H * P.B;
   const int64_t orow0 = ((int64_t)(a.out_layer ? layer : 0) * P.batch + b) * P.H * P.B;
-  for (int e = 0; e < 4; ++e) {
-    const int64_t ci = ((int64_t)part * 4 + e) * kThreads + threadIdx.x;
-    if (ci >= total) break;
-    const int ch = (int)(ci % cpr);
-    const int64_t rowi = ci / cpr;  // h * B + slot
-    const int h = (int)(rowi / P.B);
-    const int id = idx[rowi];
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (id >= 0 && id < P.T) {
+  int64_t ci[kRounds];
+  int id[kRounds];
+#pragma unroll
+  for (int e = 0; e < kRounds; ++e) {
+    ci[e] = ((int64_t)part * kRounds + e) * kThreads + threadIdx.x;
+    id[e] = ci[e] < total ? idx[ci[e] / cpr] : -1;
+  }
+  uint4 kv[kRounds], vv[kRounds];
+#pragma unroll
+  for (int e = 0; e < kRounds; ++e) {
+    kv[e] = make_uint4(0, 0, 0, 0);
+    vv[e] = make_uint4(0, 0, 0, 0);
+    if (ci[e] < total && id[e] >= 0 && id[e] < P.T) {
+      const int ch = (int)(ci[e] % cpr);
+      const int h = (int)((ci[e] / cpr) / P.B);
       const int64_t ko = ((int64_t)layer * a.ks[0] + (int64_t)b * a.ks[1] + (int64_t)h * a.ks[2] +
-                          (int64_t)id * a.ks[3]) * P.esize;
+                          (int64_t)id[e] * a.ks[3]) * P.esize;
       const int64_t vo = ((int64_t)layer * a.vs[0] + (int64_t)b * a.vs[1] + (int64_t)h * a.vs[2] +
-                          (int64_t)id * a.vs[3]) * P.esize;
-      kv = reinterpret_cast<const uint4*>(a.k + ko)[ch];
-      vv = reinterpret_cast<const uint4*>(a.v + vo)[ch];
+                          (int64_t)id[e] * a.vs[3]) * P.esize;
+      kv[e] = reinterpret_cast<const uint4*>(a.k + ko)[ch];
+      vv[e] = reinterpret_cast<const uint4*>(a.v + vo)[ch];
     }
-    const int64_t o = (orow0 + rowi) * cpr + ch;
-    reinterpret_cast<uint4*>(a.k_out)[o] = kv;
-    reinterpret_cast<uint4*>(a.v_out)[o] = vv;
+  }
+#pragma unroll
+  for (int e = 0; e < kRounds; ++e) {
+    if (ci[e] < total) {
+      const int64_t o = (orow0 + ci[e] / cpr) * cpr + ci[e] % cpr;
+      reinterpret_cast<uint4*>(a.k_out)[o] = kv[e];
+      reinterpret_cast<uint4*>(a.v_out)[o] = vv[e];
+    }
   }
 }
 

@@ -384,9 +384,9 @@ struct ScoreTile {
     // running max over heads [WR][SK + 4] (passes that can exchange), the
     // staged per-key sums of each head, and the staged importance of the tile
     const bool layout_x = part != PART_EXT && P.H > 1;
-    mbuf = smem + key_ring_bytes(ES, D) / 4 + slot * p2_slot_floats(nh, WR, P.SK, P.tile2, layout_x);
-    obuf = mbuf + (layout_x ? 2 * WR * (P.SK + 4) : 0);
-    ibuf = obuf + 2 * nh * P.tile2;
+    mbuf = smem + key_ring_bytes(ES, D) / 4 + slot * p2_slot_floats(nh, WR, P.SK, P.tile2, layout_x, P.nsum);
+    obuf = mbuf + (layout_x ? exchange_buffers(P.SK, P.tile2) * WR * (P.SK + 4) : 0);
+    ibuf = obuf + P.nsum * nh * P.tile2;
   }
 
   // Query fragments.  Padding rows (r < 0) load row 0 and inactive waves
@@ -474,8 +474,10 @@ struct ScoreTile {
       // Stage the per-key sums in LDS; they are written out after the loop so
       // that the loop issues no global stores (exact load counting).
       if (c == 0) {
-        obuf[(hs * 2 + 0) * P.tile2 + s * 16 + n] = s_all;
-        obuf[(hs * 2 + 1) * P.tile2 + s * 16 + n] = s_base;
+        // with one sum per head (no mixed tiles) the last-O sum of a base
+        // tile equals its all-row sum and is never read for other tiles
+        obuf[(hs * P.nsum) * P.tile2 + s * 16 + n] = s_all;
+        if (P.nsum == 2) obuf[(hs * 2 + 1) * P.tile2 + s * 16 + n] = s_base;
       }
       if (tile_base) {
         if (nh == 1) {
@@ -485,7 +487,8 @@ struct ScoreTile {
           // running max over the heads of this slot: p >= 0, so the float
           // order is the order of the bit patterns (ds_max_u32)
           const int kk = (s * 16) % P.SK + n;
-          unsigned* mb = reinterpret_cast<unsigned*>(mbuf) + (((s * 16) / P.SK) & 1) * WR * (P.SK + 4);
+          const int buf = exchange_buffers(P.SK, P.tile2) == 2 ? (((s * 16) / P.SK) & 1) : 0;
+          unsigned* mb = reinterpret_cast<unsigned*>(mbuf) + buf * WR * (P.SK + 4);
 #pragma unroll
           for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
@@ -508,7 +511,7 @@ struct ScoreTile {
     lds_barrier();
     if (!tile_base) return;
     const int period = (s * 16) / P.SK;
-    float* mb = mbuf + (period & 1) * WR * (P.SK + 4);
+    float* mb = mbuf + (exchange_buffers(P.SK, P.tile2) == 2 ? (period & 1) : 0) * WR * (P.SK + 4);
     const int kpw = (P.SK + nh - 1) / nh;
     const int kb0 = hs * kpw, kb1 = min(P.SK, kb0 + kpw);
     const int rg = lane >> 4;
@@ -580,9 +583,10 @@ struct ScoreTile {
       return;
     }
     if constexpr (PASS == 2) {
-      // clear both running-max buffers before any head folds rows in
+      // clear the running-max buffers before any head folds rows in
       if (exch) {
-        for (int i = lane + hs * 64; i < 2 * WR * (P.SK + 4); i += 64 * nh) mbuf[i] = 0.f;
+        const int nf = exchange_buffers(P.SK, P.tile2) * WR * (P.SK + 4);
+        for (int i = lane + hs * 64; i < nf; i += 64 * nh) mbuf[i] = 0.f;
         lds_barrier();
       }
     }
@@ -634,8 +638,8 @@ struct ScoreTile {
         for (int i = lane; i < P.tile2; i += 64) {
           const int t = ks + i;
           if (t < P.Tc) {
-            io.psum_all[o + t] = obuf[(hs * 2 + 0) * P.tile2 + i];
-            io.psum_base[o + t] = obuf[(hs * 2 + 1) * P.tile2 + i];
+            io.psum_all[o + t] = obuf[(hs * P.nsum) * P.tile2 + i];
+            io.psum_base[o + t] = obuf[(hs * P.nsum + P.nsum - 1) * P.tile2 + i];
           }
         }
         if (tile_base && hs == 0) {
