@@ -32,6 +32,7 @@ def _hip():
                                         ctypes.c_void_p]
     lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
     lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+    lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     return lib
 
 
@@ -190,28 +191,29 @@ def main():
     print("[bench] inputs resident; warming up", file=sys.stderr, flush=True)
 
     hip = _hip()
-    n_ev = kvec.kvec_profile_points(cfg)
-    evs = [_events(hip, n_ev) for _ in range(args.steps)]
+    n_launch = kvec.kvec_profile_points(cfg) - 1
+    stream = torch.cuda.current_stream().cuda_stream  # the library's stream
+    evs = _events(hip, args.steps + 1)
     for _ in range(args.warmup):
         kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    # events only between steps: a record between launches adds a few us of
+    # gap to each of them
+    assert hip.hipEventRecord(evs[0], stream) == 0
     for s in range(args.steps):
-        kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws, events=evs[s])
+        kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
+        assert hip.hipEventRecord(evs[s + 1], stream) == 0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = wall * 1e3 / args.steps
     print(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms", file=sys.stderr, flush=True)
 
-    # Duration of each fused launch of the step (HIP events on the library's
-    # stream).  In the steady state a launch does one layer's worth of every
-    # stage: pass 1 of layer j, pass 2 of j-1, pooling of j-2, candidates of
-    # j-3, the coverage selection of j-4 and the gather of j-5.
-    durs = []
-    for s in range(args.steps):
-        e = evs[s]
-        durs += [_elapsed(hip, e[i], e[i + 1]) for i in range(n_ev - 1)]
-    n_launch = n_ev - 1
+    # Average duration of a fused launch: each step's interval between HIP
+    # events on the library's stream, over its L + 10 launches (the few-us
+    # gaps between dispatches included).  In the steady state a launch does one
+    # layer's worth of every stage of the layer pipeline.
+    durs = [_elapsed(hip, evs[s], evs[s + 1]) / n_launch for s in range(args.steps)]
     avg_ms = sum(durs) / len(durs)
     es = 2 if w.dtype == "bf16" else 4
     # algorithmic bytes of the whole step: K read once, the Q window, the gather
