@@ -87,7 +87,8 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
     for (int sk = tile; sk >= (tile == kTile2Max ? 32 : 16); sk = sk == tile ? 128 : sk / 2)
       if (lds_p2(sk, tile) <= lds_cap) {
         x.tile2 = tile;
-        x.SK = sk;
+        x.SK = sk;  // a power of two
+        x.sk_shift = __builtin_ctz((unsigned)sk);
         break;
       }
   if (!x.tile2) return KVEC_ERR_UNSUPPORTED;

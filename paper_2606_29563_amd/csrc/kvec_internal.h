@@ -65,6 +65,7 @@ struct Problem {
   int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;
   float lam, sc, inv_go, inv_gwn;
   int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK, tile2;
+  int sk_shift;    // log2(SK): exchange periods are powers of two
   int nsum;        // pass-2 per-key sums per head: 1 when O is a multiple of WR (no row
                    // tile holds both last-O and earlier rows), else 2
   int n_rtg_base;  // work-groups per key tile of a BASE pass (8/H row tiles each)

@@ -430,7 +430,32 @@ struct ScoreTile {
       for (int bk = 0; bk < NB; ++bk) acc[bk] = mma1<D>(qf[bk], kf[F], acc[bk], j);
   }
 
-  template <bool MASKED>
+  // Pass-2 epilogue shapes, fixed per wave before the key loop.  EP_GEN
+  // decides per step from the tile's flags (any geometry).  With one per-key
+  // sum per head (no row tile mixes last-O and earlier rows): EP_SUM for a
+  // tile without last-O rows (the sums only), EP_IMP for a tile of last-O rows
+  // only (the sums and the max over heads, no row masked out).
+  enum { EP_GEN = 0, EP_SUM = 1, EP_IMP = 2 };
+
+  // Running max over the heads of this slot: p >= 0, so the float order is
+  // the order of the bit patterns (ds_max_u32).  Rows before rr0 (not in the
+  // last-O window) fold in a zero when ROW_MASK.
+  template <bool ROW_MASK>
+  __device__ __forceinline__ void fold_max(int s, const float (&gs)[RB][4]) {
+    const int kk = ((s * 16) & (P.SK - 1)) + n;
+    const int buf = exchange_buffers(P.SK, P.tile2) == 2 ? (((s * 16) >> P.sk_shift) & 1) : 0;
+    unsigned* mb = reinterpret_cast<unsigned*>(mbuf) + buf * WR * (P.SK + 4);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rr = rb * 16 + 4 * c + i;
+        lds_max_u32(mb + rr * (P.SK + 4) + kk,
+                    !ROW_MASK || rr >= rr0 ? __float_as_uint(gs[rb][i]) : 0u);
+      }
+  }
+
+  template <bool MASKED, int EP>
   __device__ __forceinline__ void epilogue(int s) {
     const int t = ks + 16 * s + n;
     if constexpr (PASS == 1) {
@@ -445,11 +470,9 @@ struct ScoreTile {
         }
       }
     } else {
+      // gs: sum over the G query heads of each row (p >= 0, so starting from
+      // the first term instead of 0 changes no bit)
       float gs[RB][4];
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) gs[rb][i] = 0.f;
 #pragma unroll
       for (int bk = 0; bk < NB; ++bk) {
         const int rb = bk % RB;
@@ -457,17 +480,34 @@ struct ScoreTile {
         for (int i = 0; i < 4; ++i) {
           float p = __builtin_amdgcn_exp2f(fmaf(acc[bk][i], P.sc, nlse[bk][i]));
           if constexpr (MASKED) p = t <= pos[rb][i] ? p : 0.f;
-          gs[rb][i] += p;
+          gs[rb][i] = bk < RB ? p : gs[rb][i] + p;
         }
       }
-      float s_all = 0.f, s_base = 0.f;
+      float s_all = gs[0][0];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          s_all += gs[rb][i];
-          if (tile_mixed) s_base += (r_lo + rb * 16 + 4 * c + i >= base_lo) ? gs[rb][i] : 0.f;
+        for (int i = rb == 0 ? 1 : 0; i < 4; ++i) s_all += gs[rb][i];
+      if constexpr (EP != EP_GEN) {
+        s_all = col_sum4(s_all);
+        if (c == 0) obuf[hs * P.tile2 + s * 16 + n] = s_all;
+        if constexpr (EP == EP_IMP) {
+          if (nh == 1) {
+            if (c == 0) ibuf[s * 16 + n] = s_all;
+          } else {
+            fold_max<false>(s, gs);
+          }
         }
+        return;
+      }
+      float s_base = 0.f;
+      if (tile_mixed) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            s_base += (r_lo + rb * 16 + 4 * c + i >= base_lo) ? gs[rb][i] : 0.f;
+      }
       if (tile_base && !tile_mixed) s_base = s_all;
       s_all = col_sum4(s_all);
       s_base = col_sum4(s_base);
@@ -484,19 +524,7 @@ struct ScoreTile {
           // one head: the max over heads is the head itself
           if (c == 0) ibuf[s * 16 + n] = s_base;
         } else {
-          // running max over the heads of this slot: p >= 0, so the float
-          // order is the order of the bit patterns (ds_max_u32)
-          const int kk = (s * 16) % P.SK + n;
-          const int buf = exchange_buffers(P.SK, P.tile2) == 2 ? (((s * 16) / P.SK) & 1) : 0;
-          unsigned* mb = reinterpret_cast<unsigned*>(mbuf) + buf * WR * (P.SK + 4);
-#pragma unroll
-          for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              // rows before rr0 (not in the last-O window) fold in a zero
-              const int rr = rb * 16 + 4 * c + i;
-              lds_max_u32(mb + rr * (P.SK + 4) + kk, rr >= rr0 ? __float_as_uint(gs[rb][i]) : 0u);
-            }
+          fold_max<true>(s, gs);
         }
       }
     }
@@ -510,7 +538,7 @@ struct ScoreTile {
   __device__ __forceinline__ void exchange(int s) {
     lds_barrier();
     if (!tile_base) return;
-    const int period = (s * 16) / P.SK;
+    const int period = (s * 16) >> P.sk_shift;
     float* mb = mbuf + (exchange_buffers(P.SK, P.tile2) == 2 ? (period & 1) : 0) * WR * (P.SK + 4);
     const int kpw = (P.SK + nh - 1) / nh;
     const int kb0 = hs * kpw, kb1 = min(P.SK, kb0 + kpw);
@@ -540,7 +568,7 @@ struct ScoreTile {
   // then the copy of step s + kAhead, the read of step s + 1's fragment once
   // its copy has landed, and the exponentials of step s while that read is in
   // flight.  u is the slot of step s + 1.
-  template <int F, bool TILE_MASKED>
+  template <int F, bool TILE_MASKED, int EP>
   __device__ __forceinline__ void step(int s, int u) {
     mma_frag<F>();
     const int ua = KR::R > 1 ? (u + kAhead - 1) % KR::R : 0;
@@ -551,29 +579,37 @@ struct ScoreTile {
     if constexpr (TILE_MASKED) {
       const int t0 = ks + 16 * s;
       if (t0 + 15 > lim_min || (PASS == 1 && t0 + 16 > ke))
-        epilogue<true>(s);
+        epilogue<true, EP>(s);
       else
-        epilogue<false>(s);
+        epilogue<false, EP>(s);
     } else {
-      epilogue<false>(s);
+      epilogue<false, EP>(s);
     }
     if constexpr (PASS == 2) {
-      if (exch && ((s + 1) * 16) % P.SK == 0) exchange(s);
+      if (exch && (((s + 1) * 16) & (P.SK - 1)) == 0) exchange(s);
     }
     // Keep the steps in program order (the next step's waits stay after
     // this step's work).
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  template <bool TILE_MASKED>
+  template <bool TILE_MASKED, int EP>
   __device__ __forceinline__ void run() {
     int u = KR::R > 1 ? 1 : 0;  // slot of step s + 1
     for (int s = 0; s < nsteps; s += 2) {
-      step<0, TILE_MASKED>(s, u);
+      step<0, TILE_MASKED, EP>(s, u);
       u = u + 1 == KR::R ? 0 : u + 1;
-      step<1, TILE_MASKED>(s + 1, u);
+      step<1, TILE_MASKED, EP>(s + 1, u);
       u = u + 1 == KR::R ? 0 : u + 1;
     }
+  }
+
+  template <int EP>
+  __device__ __forceinline__ void run_ep(bool masked) {
+    if (masked)
+      run<true, EP>();
+    else
+      run<false, EP>();
   }
 
   __device__ __forceinline__ void execute() {
@@ -623,10 +659,16 @@ struct ScoreTile {
     // Only tiles that reach the causal edge, T or their own end need masks;
     // every other tile runs a loop without any masking code.
     const int last_t0 = ks + 16 * (nsteps - 1);
-    if (last_t0 + 15 > lim_min || (PASS == 1 && last_t0 + 16 > ke))
-      run<true>();
-    else
-      run<false>();
+    const bool masked = last_t0 + 15 > lim_min || (PASS == 1 && last_t0 + 16 > ke);
+    if constexpr (PASS == 1) {
+      run_ep<EP_GEN>(masked);
+    } else if (P.nsum == 1 && !tile_base) {
+      run_ep<EP_SUM>(masked);
+    } else if (P.nsum == 1 && !tile_mixed) {
+      run_ep<EP_IMP>(masked);
+    } else {
+      run_ep<EP_GEN>(masked);
+    }
     finish();
   }
 
