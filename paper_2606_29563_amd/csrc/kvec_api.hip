@@ -127,7 +127,7 @@ Workspace make_workspace(const Geometry& g) {
   w.imp = take(bt * tc * 4);
   w.pooled = take(bt * P.H * tc * 4);
   w.pooled_ext = take(bt * P.H * tc * 4);
-  w.stats = take(bt * P.H * P.n_pool * 16);
+  w.stats = take(bt * P.H * pool_groups(P) * 16);
   w.hist = take(bt * 2 * P.H * kHistBins * 4);
   w.mem_t = take(bt * P.H * tc * 4);
   w.mem_ps = take(bt * P.H * tc * 4);
@@ -146,7 +146,7 @@ Workspace make_workspace(const Geometry& g) {
   const size_t p2_ext =
       P.delta_eff > 0 ? (size_t)P.tpw_x * p2_slot_floats(P.delta_eff, P.WR, P.SK, P.tile2, false, P.nsum) : 0;
   const size_t lds_p2 = key_ring_bytes(P.esize, P.D) + (p2_all > p2_ext ? p2_all : p2_ext) * 4;
-  const size_t lds_pool = (size_t)(2 * (kPoolPer * kPoolChunk + 64) + 2 * kHistBins) * 4;
+  const size_t lds_pool = (size_t)(2 * (kPoolPer * kPoolChunk + 64) + 2 * kHistBins) * 4 + kPoolPer * 16;
   const size_t lds_prep = 256;
   const size_t lds_sel = 2048 * 4 + 32 * 4 + (size_t)((P.n_prep + 1 + 3) & ~3) * 4 +
                          (size_t)16 * P.mcap;

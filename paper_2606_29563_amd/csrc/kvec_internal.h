@@ -172,37 +172,45 @@ __device__ __forceinline__ int block_excl_scan(int v, int* tmp, int& total) {
   return r;
 }
 
+// Pool work-groups per (sequence, head): each writes one float64 (sum, sum
+// of squares) of pooled P over its chunks.
+__host__ __device__ inline int pool_groups(const Problem& P) { return (P.n_pool + kPoolPer - 1) / kPoolPer; }
+
 // H_top (Sec. 4.1): bit h set for the delta_eff heads of sequence b with the
-// lowest variance of pooled P (ties: lower head), from the per-chunk float64
-// sums of the pool stage.  Every caller computes it the same way, so the
-// score passes of the extended window and the selection agree.  Work-group
-// cooperative (barriers); `vars` holds 8 doubles of shared memory.
-__device__ __forceinline__ uint32_t htop_mask(const Problem& P, const double2* stats, int b,
-                                              double* vars) {
-  // wave g sums head g's per-chunk partials (lane-strided, then a wave sum)
-  const int g = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (g < P.H) {
-    double a1 = 0.0, a2 = 0.0;
-    for (int i = lane; i < P.n_pool; i += 64) {
-      const double2 v = stats[((int64_t)b * P.H + g) * P.n_pool + i];
+// lowest variance of pooled P (ties: lower head), from the per-work-group
+// float64 sums of the pool stage.  Every caller computes it the same way, so
+// the score passes of the extended window and the selection agree.  Each wave
+// computes it on its own (no LDS, no barrier): a power-of-two group of lanes
+// per head adds that head's partials (lane-strided, then a butterfly within
+// the group), and each head's rank comes from the group leaders' variances.
+__device__ __forceinline__ uint32_t htop_mask(const Problem& P, const double2* stats, int b) {
+  const int lane = threadIdx.x & 63;
+  const int lph = P.H > 4 ? 8 : P.H > 2 ? 16 : P.H > 1 ? 32 : 64;  // lanes per head
+  const int h = lane / lph, j = lane % lph;
+  const int ng = pool_groups(P);
+  double a1 = 0.0, a2 = 0.0;
+  if (h < P.H) {
+    const double2* sh = stats + ((int64_t)b * P.H + h) * ng;
+    for (int i = j; i < ng; i += lph) {
+      const double2 v = sh[i];
       a1 += v.x;
       a2 += v.y;
     }
-    a1 = wave_sum(a1);
-    a2 = wave_sum(a2);
-    if (lane == 0) {
-      const double mean = a1 / P.Tc;
-      vars[g] = a2 / P.Tc - mean * mean;
-    }
   }
-  __syncthreads();
+  for (int o = 1; o < lph; o <<= 1) {
+    a1 += __shfl_xor(a1, o);
+    a2 += __shfl_xor(a2, o);
+  }
+  const double mean = a1 / P.Tc;
+  const double var = a2 / P.Tc - mean * mean;
+  int rank = 0;
+  for (int o = 0; o < P.H; ++o) {
+    const double vo = __shfl(var, o * lph);
+    rank += (vo < var) || (vo == var && o < h);
+  }
+  const uint64_t sel = __ballot(h < P.H && j == 0 && rank < P.delta_eff);
   uint32_t m = 0;
-  for (int h = 0; h < P.H; ++h) {
-    int rank = 0;
-    for (int o = 0; o < P.H; ++o) rank += (vars[o] < vars[h]) || (vars[o] == vars[h] && o < h);
-    m |= (uint32_t)(rank < P.delta_eff) << h;
-  }
-  __syncthreads();
+  for (int g = 0; g < P.H; ++g) m |= (uint32_t)((sel >> (g * lph)) & 1ull) << g;
   return m;
 }
 

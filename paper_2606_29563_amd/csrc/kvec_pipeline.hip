@@ -187,7 +187,6 @@ __host__ __device__ inline int lse_tasks_per_seq(const Problem& P, int st) {
 template <class TT, int D, int G>
 __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
   extern __shared__ __align__(16) char smem[];
-  __shared__ double s_var[8];  // H_top of the extended-window stages
   const Problem P = a.P;
   int blk = blockIdx.x;
   int st = 0;
@@ -229,7 +228,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int per_b = P.n_kt1 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
       const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b, s_var) : 0u;
+          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b) : 0u;
       score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot), b, rem / n_rtg, rem % n_rtg,
                               reinterpret_cast<float*>(smem), part, hm);
       break;
@@ -248,7 +247,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
         task_lse<TT, D, G>(P, io, b, blk % per_b, rb0, P.Wn - rb0, all);
       else
         task_lse<TT, D, G>(P, io, b, blk % per_b, 0, rb0,
-                           htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b, s_var));
+                           htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b));
       break;
     }
     case ST_PASS2:
@@ -260,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int b = blk / per_b, rem = blk % per_b;
       const ScoreIO io = score_io(a, sg.layer, sg.slot);
       const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b, s_var) : 0u;
+          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b) : 0u;
       score_tile<TT, D, G, 2>(P, io, b, rem / n_rtg, rem % n_rtg, reinterpret_cast<float*>(smem),
                               part, hm);
       if (part != PART_EXT) {
@@ -297,7 +296,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int per_b = P.delta_eff * nt;
       const int b = blk / per_b, rem = blk % per_b;
       const SelectIO io = select_io(a, sg.layer, sg.slot);
-      const int h = nth_bit(htop_mask(P, io.stats, b, s_var), rem / nt);
+      const int h = nth_bit(htop_mask(P, io.stats, b), rem / nt);
       const int c0 = (rem % nt) * kPoolPer;
       if (h >= 0) task_pool(P, io, b, h, c0, min(P.n_pool, c0 + kPoolPer), smem, false, true);
       break;

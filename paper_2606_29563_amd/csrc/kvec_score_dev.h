@@ -246,6 +246,8 @@ struct ScoreIO {
 // Word 3 of a raw buffer resource on the gfx9 family (32-bit data format,
 // no swizzle); loads outside num_records return zero.
 constexpr int kBufferWord3 = 0x00020000;
+// A vector offset past every buffer of the score passes (num_records < 2^31).
+constexpr int kOutOfRange = (int)0x80000000u;
 
 // Per-wave LDS ring of key steps (16 keys per step).
 template <class TT, int D>
@@ -347,8 +349,7 @@ struct ScoreTile {
     ring = reinterpret_cast<uint4*>(smem) + w * (KR::R * KR::SLOT / 16);
     // Steps are padded to an even count (the loop alternates two fragment
     // registers) and, in pass 2, to the importance exchange; keys at or past
-    // ke are masked (pass 1) or never stored (pass 2), and keys past tend read
-    // as zero.
+    // ke read as zero and are masked (pass 1) or never stored (pass 2).
     nsteps = (ke - ks + 15) / 16;
     const int pad = PASS == 2 ? max(2, P.SK / 16) : 2;
     nsteps = (nsteps + pad - 1) / pad * pad;
@@ -405,12 +406,28 @@ struct ScoreTile {
 
   // Copy the 16 keys of step st into ring slot u (lane l writes 16 bytes at
   // l * 16 of each 1 KiB load; its global piece is pre-swizzled in voff).
+  // A step whose keys all lie in [ks, ke) passes the step offset in the
+  // scalar offset.  Any other step (the tile's ragged end, padding steps and
+  // the copies issued ahead past the last step) moves the whole offset into
+  // the vector offset, which the buffer range check covers, and points keys
+  // outside the tile past the end of the buffer: those read as zero without
+  // touching memory, and the number of copies in flight stays the same.
   __device__ __forceinline__ void dma(int u, int st) {
     auto* dst = (__attribute__((address_space(3))) char*)(reinterpret_cast<char*>(ring) + u * KR::SLOT);
-    const int soff = (ks + 16 * st) * kstride;
+    const int k0 = ks + 16 * st;
+    if (k0 + 16 <= ke) {
+      const int soff = k0 * kstride;
 #pragma unroll
-    for (int i = 0; i < KR::NI; ++i)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, voff[i], soff, 0, 0);
+      for (int i = 0; i < KR::NI; ++i)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, voff[i], soff, 0, 0);
+    } else {
+#pragma unroll
+      for (int i = 0; i < KR::NI; ++i) {
+        const int kk = k0 + i * KR::KPI + lane / KR::CPR;
+        const int off = kk < ke ? voff[i] + k0 * kstride : kOutOfRange;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, off, 0, 0, 0);
+      }
+    }
   }
 
   template <int F>

@@ -84,6 +84,7 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
   float* se = sp + (kPoolPer * kPoolChunk + 64);      // raw P'  [a0, a1)
   uint32_t* hp = reinterpret_cast<uint32_t*>(se + (kPoolPer * kPoolChunk + 64));
   uint32_t* he = hp + kHistBins;
+  double2* wst = reinterpret_cast<double2*>(he + kHistBins);  // [kPoolPer] chunk sums
   for (int i = threadIdx.x; i < 2 * kHistBins; i += blockDim.x) hp[i] = 0u;
   const int64_t row = ((int64_t)b * P.H + h) * P.Tc;
   // The window is at most kPoolPer * kPoolChunk + 62 tokens: kSpan loads per
@@ -189,10 +190,19 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
     if (want_p) {
       s1 = wave_sum(s1);
       s2 = wave_sum(s2);
-      if (lane == 0) io.stats[((int64_t)b * P.H + h) * P.n_pool + chunk] = make_double2(s1, s2);
+      if (lane == 0) wst[w] = make_double2(s1, s2);
     }
   }
   __syncthreads();
+  if (want_p && threadIdx.x == 0) {
+    // one (sum, sum of squares) per work-group: its chunks added in order
+    double s1 = 0.0, s2 = 0.0;
+    for (int k = 0; k < c1 - c0; ++k) {
+      s1 += wst[k].x;
+      s2 += wst[k].y;
+    }
+    io.stats[((int64_t)b * P.H + h) * pool_groups(P) + c0 / kPoolPer] = make_double2(s1, s2);
+  }
   uint32_t* gh = io.hist + ((int64_t)b * 2 * P.H) * kHistBins;
   for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
     if (hp[i]) atomicAdd(&gh[(int64_t)h * kHistBins + i], hp[i]);
@@ -210,8 +220,7 @@ __device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, 
     uint64_t* row = io.bits + ((int64_t)b * P.L + layer) * P.words;
     for (int i = threadIdx.x; i < P.words; i += blockDim.x) row[i] = 0ull;
   }
-  double* var = reinterpret_cast<double*>(smem);
-  int* tmp = reinterpret_cast<int*>(var + 8);
+  int* tmp = reinterpret_cast<int*>(smem);
   // Every load is issued before H_top is known (one memory round trip):
   // both histograms of head h, and both pooled scores and I of this wave's
   // chunk (wave w extracts chunk c0 + w; round k covers tokens
@@ -242,7 +251,7 @@ __device__ __forceinline__ void task_prep(const Problem& P, const SelectIO& io, 
     pe[k] = io.pooled_ext[hrow + t];
     im[k] = imp[t];
   }
-  const uint32_t top = htop_mask(P, io.stats, b, var);
+  const uint32_t top = htop_mask(P, io.stats, b);
   if (h == 0 && c0 == 0 && threadIdx.x == 0 && io.htop_mask) io.htop_mask[b] = top;
   const bool ext = (top >> h) & 1u;
   // Bins holding the Kp-th and the M-th largest key, from one descending
