@@ -404,14 +404,18 @@ __device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io
   char* marr = reinterpret_cast<char*>(off + ((P.n_prep + 1 + 3) & ~3));
   const int64_t hb = (int64_t)b * P.H + h;
   const int32_t* mn = io.mem_n + hb * P.n_prep;
-  // member offsets of the prep chunks
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int c = 0; c < P.n_prep; ++c) {
-      off[c] = acc;
-      acc += mn[c];
+  // member offsets of the prep chunks (wave 0, 64 chunks per round)
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    int carry = 0;
+    for (int c0 = 0; c0 < P.n_prep; c0 += 64) {
+      const int c = c0 + lane;
+      const int v = c < P.n_prep ? mn[c] : 0;
+      const int incl = wave_incl_scan(v);
+      if (c < P.n_prep) off[c] = carry + incl - v;
+      carry += __shfl(incl, 63);
     }
-    off[P.n_prep] = acc;
+    if (lane == 0) off[P.n_prep] = carry;
   }
   __syncthreads();
   const int n = off[P.n_prep];
@@ -429,19 +433,43 @@ __device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io
     mp = io.spill_ps + hb * P.Tc;
     mi = io.spill_i + hb * P.Tc;
   }
-  // gather the members contiguously (ascending t), with their preserve keys
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    int lo = 0, hi = P.n_prep - 1;  // chunk c with off[c] <= i < off[c+1]
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (off[mid] <= i) lo = mid; else hi = mid - 1;
+  // gather the members contiguously (ascending t), with their preserve keys;
+  // kBatch members per thread have their loads in flight together
+  constexpr int kBatch = 8;
+  const int32_t* gt = io.mem_t + hb * P.Tc;
+  const float* gp = io.mem_ps + hb * P.Tc;
+  const float* gi = io.mem_i + hb * P.Tc;
+  for (int i0 = threadIdx.x; i0 < n; i0 += kBatch * blockDim.x) {
+    int g[kBatch];  // member position in the head's chunk arrays
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = i0 + u * (int)blockDim.x;
+      int lo = 0, hi = P.n_prep - 1;  // chunk c with off[c] <= i < off[c+1]
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (off[mid] <= i) lo = mid; else hi = mid - 1;
+      }
+      g[u] = lo * kPrepChunk + (i - off[lo]);
     }
-    const int64_t g = hb * P.Tc + (int64_t)lo * kPrepChunk + (i - off[lo]);
-    const float ps = io.mem_ps[g];
-    mt[i] = io.mem_t[g];
-    mp[i] = ps;
-    mi[i] = io.mem_i[g];
-    kb[i] = float_key(ps);
+    int32_t vt[kBatch];
+    float vp[kBatch], vi[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const bool ok = i0 + u * (int)blockDim.x < n;
+      vt[u] = ok ? gt[g[u]] : 0;
+      vp[u] = ok ? gp[g[u]] : 0.f;
+      vi[u] = ok ? gi[g[u]] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = i0 + u * (int)blockDim.x;
+      if (i < n) {
+        mt[i] = vt[u];
+        mp[i] = vp[u];
+        mi[i] = vi[u];
+        kb[i] = float_key(vp[u]);
+      }
+    }
   }
   __syncthreads();
   // 1. preserve set: first Kp members by (P_sel desc, t asc)
