@@ -145,16 +145,34 @@ __device__ __forceinline__ float dpp_f(float v) {
 constexpr int kDppSwap1 = 0xB1;        // quad_perm [1,0,3,2]
 constexpr int kDppSwap2 = 0x4E;        // quad_perm [2,3,0,1]
 constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppRor8 = 0x128;        // row_ror:8 (lane n <-> n ^ 8 within a row)
 constexpr int kDppMirror = 0x140;      // row_mirror
 
-// Sum over the 16 lanes of each row; every lane of the row gets the same sum.
-__device__ __forceinline__ float row_sum16(float v) {
-  v += dpp_f<kDppSwap1>(v);
-  v += dpp_f<kDppSwap2>(v);
-  v += dpp_f<kDppHalfMirror>(v);
-  v += dpp_f<kDppMirror>(v);
-  return v;
+// Transpose-reduce over the 16 lanes of each DPP row: v<k> holds a lane's
+// term of quantity k (k < 16); afterwards lane n of the row returns the row
+// total of quantity n.  Four exchange rounds pair lanes 8 apart, mirrored
+// within 8, 2 apart and 1 apart; in each, a lane keeps the half of its
+// quantities that its side of the pair owns and adds the partner's terms of
+// that half (15 lane moves for 16 sums instead of 64).  Written on scalars:
+// the selects must stay selects of values, not of array elements.
+template <int CTRL>
+__device__ __forceinline__ float xchg_keep(bool up, float lo, float hi) {
+  return (up ? hi : lo) + dpp_f<CTRL>(up ? lo : hi);
 }
+__device__ __forceinline__ float row_transpose_sum16(
+    int n, float v0, float v1, float v2, float v3, float v4, float v5, float v6, float v7,
+    float v8, float v9, float v10, float v11, float v12, float v13, float v14, float v15) {
+  const bool u8 = (n & 8) != 0, u4 = (n & 4) != 0, u2 = (n & 2) != 0, u1 = (n & 1) != 0;
+  const float a0 = xchg_keep<kDppRor8>(u8, v0, v8), a1 = xchg_keep<kDppRor8>(u8, v1, v9);
+  const float a2 = xchg_keep<kDppRor8>(u8, v2, v10), a3 = xchg_keep<kDppRor8>(u8, v3, v11);
+  const float a4 = xchg_keep<kDppRor8>(u8, v4, v12), a5 = xchg_keep<kDppRor8>(u8, v5, v13);
+  const float a6 = xchg_keep<kDppRor8>(u8, v6, v14), a7 = xchg_keep<kDppRor8>(u8, v7, v15);
+  const float b0 = xchg_keep<kDppHalfMirror>(u4, a0, a4), b1 = xchg_keep<kDppHalfMirror>(u4, a1, a5);
+  const float b2 = xchg_keep<kDppHalfMirror>(u4, a2, a6), b3 = xchg_keep<kDppHalfMirror>(u4, a3, a7);
+  const float c0 = xchg_keep<kDppSwap2>(u2, b0, b2), c1 = xchg_keep<kDppSwap2>(u2, b1, b3);
+  return xchg_keep<kDppSwap1>(u1, c0, c1);
+}
+
 __device__ __forceinline__ float row_max16(float v) {
   v = fmaxf(v, dpp_f<kDppSwap1>(v));
   v = fmaxf(v, dpp_f<kDppSwap2>(v));
@@ -689,6 +707,31 @@ struct ScoreTile {
     finish();
   }
 
+  // Pass 1: the (reference, sum) partials of blocks Q0 .. Q0 + 3 of this key
+  // tile, one store for the wave (compile-time indices only, so the sums stay
+  // in registers).
+  template <int Q0>
+  __device__ __forceinline__ void store_partials() {
+    float l = row_transpose_sum16(
+        n, lsum[Q0][0], lsum[Q0][1], lsum[Q0][2], lsum[Q0][3], lsum[Q0 + 1][0], lsum[Q0 + 1][1],
+        lsum[Q0 + 1][2], lsum[Q0 + 1][3], lsum[Q0 + 2][0], lsum[Q0 + 2][1], lsum[Q0 + 2][2],
+        lsum[Q0 + 2][3], lsum[Q0 + 3][0], lsum[Q0 + 3][1], lsum[Q0 + 3][2], lsum[Q0 + 3][3]);
+    const int bq = n >> 2, i = n & 3;
+    const int bk = Q0 + bq;
+    const int g = bk / RB, rb = bk % RB;
+    const int j = h * G + g;
+    const int r = r_lo + rb * 16 + 4 * c + i;
+    const float m0 = mref[Q0], m1 = mref[Q0 + 1], m2 = mref[Q0 + 2], m3 = mref[Q0 + 3];
+    const float mb = bq == 0 ? m0 : bq == 1 ? m1 : bq == 2 ? m2 : m3;
+    // rows past the tile's first key hold no valid key here: (-inf, 0)
+    const bool has_keys = ks <= P.T - P.Wn + r;
+    const float m = has_keys ? mb : -INFINITY;
+    if (!has_keys) l = 0.f;
+    else if (!(l >= 0x1p-64f && l < INFINITY)) l = INFINITY;  // exact recompute
+    if (active && r >= 0)
+      io.lse_part[(((int64_t)b * P.HQ + j) * P.Wn + r) * P.n_kt1 + kt] = make_float2(m, l);
+  }
+
   __device__ __forceinline__ void finish() {
     if constexpr (PASS == 2) {
       lds_barrier();
@@ -709,23 +752,11 @@ struct ScoreTile {
         }
       }
     } else {
-#pragma unroll
-      for (int bk = 0; bk < NB; ++bk) {
-        const int g = bk / RB, rb = bk % RB;
-        const int j = h * G + g;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float l = row_sum16(lsum[bk][i]);
-          const int r = r_lo + rb * 16 + 4 * c + i;
-          // rows past the tile's first key hold no valid key here: (-inf, 0)
-          const bool has_keys = ks <= pos[rb][i];
-          float m = has_keys ? mref[bk] : -INFINITY;
-          if (!has_keys) l = 0.f;
-          else if (!(l >= 0x1p-64f && l < INFINITY)) l = INFINITY;  // exact recompute
-          if (active && n == 0 && r >= 0)
-            io.lse_part[(((int64_t)b * P.HQ + j) * P.Wn + r) * P.n_kt1 + kt] = make_float2(m, l);
-        }
-      }
+      // Row sums of 4 blocks (16 quantities: block, row of the lane group) at a
+      // time; lane n of each row ends with quantity n and stores its partial.
+      static_assert(NB == 4 || NB == 8, "blocks in groups of four");
+      store_partials<0>();
+      if constexpr (NB == 8) store_partials<4>();
     }
   }
 };
