@@ -126,6 +126,54 @@ def measured_traffic(workload: str):
         return None
 
 
+def prefill_lse(q, k, w):
+    """The window rows' log-sum-exp that the layer's prefill attention hands over
+    (input preparation for kvec_evict_model_lse, not timed): fp32 causal
+    logsumexp of q . k / sqrt(d) over keys 0..p of each window row, with torch
+    on the device.  Returns [L][b][HQ][Wn] fp32."""
+    import math
+
+    import torch
+    L, b, HQ, Wn, d = q.shape
+    G = HQ // k.shape[2]
+    T = k.shape[3]
+    pos = T - Wn + torch.arange(Wn, device=q.device)
+    hidden = torch.arange(T, device=q.device)[None, :] > pos[:, None]     # [Wn][T]
+    out = torch.empty((L, b, HQ, Wn), dtype=torch.float32, device=q.device)
+    for l in range(L):
+        for s in range(b):
+            kt = k[l, s].float().transpose(1, 2).contiguous()              # [H][d][T]
+            for j0 in range(0, HQ, G):
+                qs = q[l, s, j0:j0 + G].float()                             # [G][Wn][d]
+                lg = torch.matmul(qs, kt[j0 // G]) / math.sqrt(d)            # [G][Wn][T]
+                lg.masked_fill_(hidden, float("-inf"))
+                out[l, s, j0:j0 + G] = torch.logsumexp(lg, dim=-1)
+    return out
+
+
+def time_steps(hip, stream, run, steps: int, warmup: int):
+    """Per-step durations (ms) between HIP events at the step boundaries, and
+    the host wall time (ms) of the timed steps."""
+    import torch
+    evs = _events(hip, steps + 1)
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    # events only between steps: a record between launches adds a few us of
+    # gap to each of them
+    assert hip.hipEventRecord(evs[0], stream) == 0
+    for s in range(steps):
+        run()
+        assert hip.hipEventRecord(evs[s + 1], stream) == 0
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) * 1e3
+    durs = [_elapsed(hip, evs[s], evs[s + 1]) for s in range(steps)]
+    for e in evs:
+        hip.hipEventDestroy(e)
+    return durs, wall
+
+
 def copy_calibration(mib: int) -> None:
     """A plain device copy of known size, to scale the HBM byte counters."""
     import torch
@@ -146,6 +194,10 @@ def main():
     ap.add_argument("--workload", type=int, default=2, help="index of the synthetic workload")
     ap.add_argument("--cpu-sample-layers", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", choices=("both", "model", "lse"), default="both",
+                    help="model: kvec_evict_model only; lse: kvec_evict_model_lse only "
+                         "(row normalisers from the prefill); both: the headline plus the "
+                         "given-lse step as a second object")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -191,41 +243,58 @@ def main():
     print("[bench] inputs resident; warming up", file=sys.stderr, flush=True)
 
     hip = _hip()
-    n_launch = kvec.kvec_profile_points(cfg) - 1
     stream = torch.cuda.current_stream().cuda_stream  # the library's stream
-    evs = _events(hip, args.steps + 1)
-    for _ in range(args.warmup):
-        kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    # events only between steps: a record between launches adds a few us of
-    # gap to each of them
-    assert hip.hipEventRecord(evs[0], stream) == 0
-    for s in range(args.steps):
-        kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
-        assert hip.hipEventRecord(evs[s + 1], stream) == 0
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_step = wall * 1e3 / args.steps
-    print(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms", file=sys.stderr, flush=True)
-
-    # Average duration of a fused launch: each step's interval between HIP
-    # events on the library's stream, over its L + 10 launches (the few-us
-    # gaps between dispatches included).  In the steady state a launch does one
-    # layer's worth of every stage of the layer pipeline.
-    durs = [_elapsed(hip, evs[s], evs[s + 1]) / n_launch for s in range(args.steps)]
-    avg_ms = sum(durs) / len(durs)
     es = 2 if w.dtype == "bf16" else 4
     # algorithmic bytes of the whole step: K read once, the Q window, the gather
     # (read and write of the kept K and V rows)
     step_bytes = L * b * (H * T * d * es + HQ * w.rows * d * es + 4 * H * B * d * es)
-    per_launch = step_bytes / n_launch
-    achieved = per_launch / (avg_ms * 1e-3) / 1e9
-    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(w.name),
-            "kernel": "step_kernel (fused pipeline launch)", "launches_per_step": n_launch,
-            "avg_launch_us": round(avg_ms * 1e3, 2),
-            "algorithmic_bytes_per_launch": int(per_launch)}
+    tokens = b * T
+
+    def roofline(durs, n_launch, traffic):
+        # Average duration of a fused launch: each step's interval between HIP
+        # events on the library's stream, over its launches (the few-us gaps
+        # between dispatches included).  In the steady state a launch does one
+        # layer's worth of every stage of the layer pipeline.
+        avg_ms = sum(durs) / len(durs) / n_launch
+        per_launch = step_bytes / n_launch
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": "step_kernel (fused pipeline launch)", "launches_per_step": n_launch,
+                "avg_launch_us": round(avg_ms * 1e3, 2),
+                "algorithmic_bytes_per_launch": int(per_launch)}
+
+    roof = ms_step = None
+    if args.path in ("both", "model"):
+        n_launch = kvec.kvec_profile_points(cfg) - 1
+        durs, wall = time_steps(
+            hip, stream, lambda: kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws),
+            args.steps, args.warmup)
+        ms_step = wall / args.steps
+        print(f"[bench] {args.steps} steps in {wall:.2f} ms", file=sys.stderr, flush=True)
+        roof = roofline(durs, n_launch, measured_traffic(w.name))
+
+    lse_obj = None
+    if args.path in ("both", "lse"):
+        print("[bench] window-row log-sum-exp (prefill attention stand-in)", file=sys.stderr,
+              flush=True)
+        lse = prefill_lse(q, k, w)
+        n_launch = kvec.kvec_profile_points_lse(cfg) - 1
+        durs, wall = time_steps(
+            hip, stream,
+            lambda: kvec.kvec_evict_model_lse(cfg, q, lse, k, v, bits, idx, ko, vo, ws),
+            args.steps, args.warmup)
+        print(f"[bench] given-lse: {args.steps} steps in {wall:.2f} ms", file=sys.stderr,
+              flush=True)
+        ms_lse = wall / args.steps
+        lse_obj = {"entry": "kvec_evict_model_lse",
+                   "what": "the same step with the window rows' log-sum-exp handed over by the "
+                           "layer's prefill attention (one score pass over K instead of two)",
+                   "value": round(tokens / (ms_lse * 1e-3), 1), "unit": "prefix tokens/s",
+                   "ms_per_step": round(ms_lse, 4),
+                   "roofline": roofline(durs, n_launch, measured_traffic(w.name + "-lse"))}
+        if roof is None:
+            roof, ms_step = lse_obj["roofline"], ms_lse
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -234,7 +303,6 @@ def main():
         print(f"[bench] CPU oracle on {sample} layer(s)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, sample)
 
-    tokens = b * T
     out = {
         "metric": "prefix tokens/s through full eviction step (all layers); % HBM/MFMA roofline",
         "value": round(tokens / (ms_step * 1e-3), 1), "unit": "prefix tokens/s", "n_gpus": 1,
@@ -248,6 +316,10 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
     }
+    if args.path == "lse":
+        out["config"]["entry"] = "kvec_evict_model_lse"
+    elif lse_obj is not None:
+        out["prefill_lse_step"] = lse_obj
     print(json.dumps(out))
 
 

@@ -24,6 +24,12 @@
  *   kvec_evict_model  the whole prefill eviction step for all layers.
  *   kvec_coverage     the coverage C = number of unique tokens kept across
  *                     heads and layers (Sec. 3.2).
+ *   kvec_score_lse, kvec_evict_model_lse
+ *                     the same scores and step when the caller already holds
+ *                     the softmax normaliser of every window row: K-VEC runs
+ *                     inside the prefill of each layer (Sec. 5.1), whose
+ *                     attention computes that log-sum-exp for all query rows,
+ *                     so the scores then need one pass over K instead of two.
  *
  * Conventions common to every call
  *   - Heads are KV heads.  Query head j belongs to KV head j / G with
@@ -109,6 +115,24 @@ kvec_status kvec_score(const kvec_config* cfg,
                        float* p_raw, float* p_ext_raw, float* imp,
                        void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Window scores of one layer, as kvec_score, from the caller's row
+ * normalisers (the log-sum-exp the layer's prefill attention computed for
+ * its query rows; Sec. 4.1 Eq. eviction divides by exactly this sum).
+ *   lse          device, fp32 [batch][n_q_heads][O'] with strides
+ *                lse_strides = {batch, head} in elements and rows contiguous;
+ *                lse[b][j][r] = ln sum_{t <= T-O'+r} exp(q_{b,j,r} . k_{b,j/G,t}
+ *                / sqrt(d)), natural log, over the same causal keys as the
+ *                scores.  4-byte aligned (else KVEC_ERR_INVALID).
+ *   other arguments, outputs and errors as kvec_score.  Only the accuracy of
+ *   lse bounds the scores' accuracy: an error e in lse scales that row's
+ *   probabilities by exp(-e). */
+kvec_status kvec_score_lse(const kvec_config* cfg,
+                           const void* q_win, const int64_t q_strides[3],
+                           const float* lse, const int64_t lse_strides[2],
+                           const void* k, const int64_t k_strides[3],
+                           float* p_raw, float* p_ext_raw, float* imp,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Selection of one layer from its scores (Algorithm 1, then top-B, Sec. 4.1-4.2).
  *   layer       0-based index l; coverage uses n_t/(l+1).
  *   p_raw, p_ext_raw, imp  device fp32, as written by kvec_score.
@@ -167,6 +191,27 @@ kvec_status kvec_evict_model(const kvec_config* cfg,
 /* Number of events kvec_evict_model records when given an event array
  * (n_layers + 11; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);
+
+/* The whole prefill eviction step, as kvec_evict_model, with the window rows'
+ * normalisers from the caller (K-VEC applied inside each layer's prefill,
+ * Sec. 5.1; see kvec_score_lse for their definition).
+ *   lse          device, fp32 [L][batch][n_q_heads][O'] with strides
+ *                lse_strides = {layer, batch, head} in elements, rows
+ *                contiguous.  Required even when T <= B (then unread).
+ *   events       nullable; else kvec_profile_points_lse(cfg) events.
+ *   other arguments, outputs and errors as kvec_evict_model. */
+kvec_status kvec_evict_model_lse(const kvec_config* cfg,
+                                 const void* q_win, const int64_t q_strides[4],
+                                 const float* lse, const int64_t lse_strides[3],
+                                 const void* k, const int64_t k_strides[4],
+                                 const void* v, const int64_t v_strides[4],
+                                 uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
+                                 void* ws, size_t ws_bytes, hipStream_t stream,
+                                 hipEvent_t* events);
+
+/* Number of events kvec_evict_model_lse records (n_layers + 7; 0 when
+ * T <= B), or -1 for an invalid configuration. */
+int32_t kvec_profile_points_lse(const kvec_config* cfg);
 
 /* Coverage C (Sec. 3.2) per sequence over layers 0..upto_layer:
  * count_per_seq[b] = popcount of the OR of those layers' bitmaps.

@@ -8,6 +8,8 @@ Source: "Coverage-Driven KV Cache Eviction for Efficient and Improved Inference
 of LLM" (K-VEC).  Each function names the passage it follows:
 
 * windowed eviction score P                      Sec. 4.1, Eq. (eviction)
+* row normaliser (log-sum-exp) of the window rows  Sec. 4.1, Eq. (eviction): the
+  softmax denominator of A; eviction runs inside each layer's prefill (Sec. 5.1)
 * top-B selection per head, cache store           Sec. 4.1 (equation after Eq. eviction)
 * head focus sigma = std of P over tokens         Sec. 4.1
 * H_top = delta heads with the LOWEST sigma,
@@ -41,7 +43,7 @@ from dataclasses import dataclass
 import numpy as np
 
 __all__ = [
-    "window_attention", "window_scores", "to_f32", "maxpool1d", "head_sigma",
+    "window_attention", "window_lse", "window_scores", "to_f32", "maxpool1d", "head_sigma",
     "adjusted_heads", "rank_first", "preserve_count", "adjusted_priority",
     "LayerResult", "select_layer", "evict_layer_from_scores", "score_layer",
     "gather_rows", "coverage_count", "counts_from_bits", "layer_bits",
@@ -77,6 +79,29 @@ def window_attention(q_win: np.ndarray, k: np.ndarray) -> np.ndarray:
             a = e / e.sum(axis=1, keepdims=True)
             out[h] += a
         out[h] /= g
+    return out
+
+
+def window_lse(q_win: np.ndarray, k: np.ndarray) -> np.ndarray:
+    """Natural-log softmax normaliser of every window row of every query head.
+
+    q_win: [H_q][Wn][d] float64 (positions T-Wn .. T-1), k: [H_kv][T][d].
+    Returns lse [H_q][Wn]: lse[j, r] = ln sum_{t <= p_r} exp(q_{j,r} . k_{j//G,t} / sqrt(d)),
+    the denominator of the causal softmax A in the eviction score (Sec. 4.1),
+    i.e. the log-sum-exp that the layer's prefill attention produces for
+    those query rows.
+    """
+    hq, wn, d = q_win.shape
+    hkv, T, _ = k.shape
+    g = hq // hkv
+    pos = T - wn + np.arange(wn)
+    visible = np.arange(T)[None, :] <= pos[:, None]
+    out = np.zeros((hq, wn))
+    for j in range(hq):
+        s = (q_win[j] @ k[j // g].T) / math.sqrt(d)
+        s = np.where(visible, s, -np.inf)
+        m = s.max(axis=1)
+        out[j] = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
     return out
 
 

@@ -181,6 +181,14 @@ bool keys_addressable(const Problem& P, int64_t t_stride) {
 
 kvec_status dev(hipError_t e) { return e == hipSuccess ? KVEC_OK : KVEC_ERR_DEVICE; }
 
+// Caller-supplied row normalisers: fp32, 4-byte aligned, non-negative strides.
+bool lse_ok(const float* lse, const int64_t* s, int n) {
+  if (!lse || ((uintptr_t)lse & 3u) != 0 || !s) return false;
+  for (int i = 0; i < n; ++i)
+    if (s[i] < 0) return false;
+  return true;
+}
+
 kvec_status check_ws(const Geometry& g, void* ws, size_t ws_bytes) {
   const Workspace w = make_workspace(g);
   if (ws_bytes < w.total) return KVEC_ERR_WORKSPACE;
@@ -221,7 +229,26 @@ kvec_status kvec_score(const kvec_config* cfg, const void* q_win, const int64_t 
   if (!keys_addressable(g.p, k_strides[2])) return KVEC_ERR_UNSUPPORTED;
   if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
   const Workspace w = make_workspace(g);
-  return dev(run_score(g, q_win, q_strides, k, k_strides, p_raw, p_ext_raw, imp,
+  return dev(run_score(g, q_win, q_strides, k, k_strides, nullptr, nullptr, p_raw, p_ext_raw, imp,
+                       static_cast<char*>(ws), w, stream));
+}
+
+kvec_status kvec_score_lse(const kvec_config* cfg, const void* q_win, const int64_t q_strides[3],
+                           const float* lse, const int64_t lse_strides[2], const void* k,
+                           const int64_t k_strides[3], float* p_raw, float* p_ext_raw, float* imp,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+  Geometry g;
+  kvec_status st = make_geometry(cfg, &g);
+  if (st != KVEC_OK) return st;
+  if (g.p.Tc < 1) return KVEC_ERR_INVALID;
+  if (!aligned16(q_win) || !aligned16(k) || !strides_ok(q_strides, 3, g.p.esize) ||
+      !strides_ok(k_strides, 3, g.p.esize) || !p_raw || !p_ext_raw || !imp)
+    return KVEC_ERR_INVALID;
+  if (!lse_ok(lse, lse_strides, 2)) return KVEC_ERR_INVALID;
+  if (!keys_addressable(g.p, k_strides[2])) return KVEC_ERR_UNSUPPORTED;
+  if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
+  const Workspace w = make_workspace(g);
+  return dev(run_score(g, q_win, q_strides, k, k_strides, lse, lse_strides, p_raw, p_ext_raw, imp,
                        static_cast<char*>(ws), w, stream));
 }
 
@@ -299,11 +326,15 @@ kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* 
   return dev(run_evict_layer(g, layer, m, static_cast<char*>(ws), w, stream));
 }
 
-kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const int64_t q_strides[4],
-                             const void* k, const int64_t k_strides[4], const void* v,
-                             const int64_t v_strides[4], uint64_t* cover_bits, int32_t* idx,
-                             void* k_out, void* v_out, void* ws, size_t ws_bytes,
-                             hipStream_t stream, hipEvent_t* events) {
+}  // extern "C"
+
+namespace {
+
+kvec_status evict_model(const kvec_config* cfg, const void* q_win, const int64_t q_strides[4],
+                        const float* lse, const int64_t lse_strides[3], const void* k,
+                        const int64_t k_strides[4], const void* v, const int64_t v_strides[4],
+                        uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out, void* ws,
+                        size_t ws_bytes, hipStream_t stream, hipEvent_t* events) {
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
@@ -330,6 +361,9 @@ kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const in
   m.idx = idx;
   m.k_out = k_out;
   m.v_out = v_out;
+  m.lse = lse;
+  if (lse)
+    for (int i = 0; i < 3; ++i) m.ls[i] = lse_strides[i];
   if (g.keep_all) {
     for (int l = 0; l < g.p.L; ++l) {
       const hipError_t e = run_keep_all(g, l, cover_bits, idx + (int64_t)l * g.p.batch * g.p.H * g.p.B,
@@ -339,6 +373,31 @@ kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const in
     return dev(run_compact(g, g.p.L, m, stream));
   }
   return dev(run_model(g, m, static_cast<char*>(ws), w, stream, events));
+}
+
+}  // namespace
+
+extern "C" {
+
+kvec_status kvec_evict_model(const kvec_config* cfg, const void* q_win, const int64_t q_strides[4],
+                             const void* k, const int64_t k_strides[4], const void* v,
+                             const int64_t v_strides[4], uint64_t* cover_bits, int32_t* idx,
+                             void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                             hipStream_t stream, hipEvent_t* events) {
+  return evict_model(cfg, q_win, q_strides, nullptr, nullptr, k, k_strides, v, v_strides, cover_bits,
+                     idx, k_out, v_out, ws, ws_bytes, stream, events);
+}
+
+kvec_status kvec_evict_model_lse(const kvec_config* cfg, const void* q_win,
+                                 const int64_t q_strides[4], const float* lse,
+                                 const int64_t lse_strides[3], const void* k,
+                                 const int64_t k_strides[4], const void* v,
+                                 const int64_t v_strides[4], uint64_t* cover_bits, int32_t* idx,
+                                 void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                                 hipStream_t stream, hipEvent_t* events) {
+  if (!lse_ok(lse, lse_strides, 3)) return KVEC_ERR_INVALID;
+  return evict_model(cfg, q_win, q_strides, lse, lse_strides, k, k_strides, v, v_strides,
+                     cover_bits, idx, k_out, v_out, ws, ws_bytes, stream, events);
 }
 
 kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, int32_t upto_layer,
@@ -355,6 +414,12 @@ int32_t kvec_profile_points(const kvec_config* cfg) {
   Geometry g;
   if (make_geometry(cfg, &g) != KVEC_OK) return -1;
   return g.keep_all ? 0 : g.p.L + kPipeDepth + 1;
+}
+
+int32_t kvec_profile_points_lse(const kvec_config* cfg) {
+  Geometry g;
+  if (make_geometry(cfg, &g) != KVEC_OK) return -1;
+  return g.keep_all ? 0 : g.p.L + kPipeDepthLse + 1;
 }
 
 const char* kvec_status_string(kvec_status s) {

@@ -11,6 +11,7 @@ namespace kvec {
 
 constexpr int kThreads = 512;  // every work-group of the step kernel: 8 waves
 constexpr int kPipeDepth = 10;         // launches between a layer's first and last stage
+constexpr int kPipeDepthLse = 6;       // the same when the row normalisers are given
 constexpr int kRing = kPipeDepth + 1;  // layers in flight in the software pipeline
 
 constexpr int kTile1 = 512;       // keys per pass-1 work-group
@@ -106,13 +107,15 @@ struct ModelIO {
   int32_t* idx;           // [L][b][H][B] (or [b][H][B] for one layer)
   void* k_out;            // [L][b][H][B][d]
   void* v_out;
+  const float* lse;       // nullable: natural-log row normalisers [layer][b][HQ][Wn], strides ls
+  int64_t ls[3];
 };
 
 hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Workspace& w,
                      hipStream_t s, hipEvent_t* ev);
 hipError_t run_score(const Geometry& g, const void* q, const int64_t qs[3], const void* k,
-                     const int64_t ks[3], float* p_raw, float* p_ext, float* imp, char* ws,
-                     const Workspace& w, hipStream_t s);
+                     const int64_t ks[3], const float* lse, const int64_t ls[2], float* p_raw,
+                     float* p_ext, float* imp, char* ws, const Workspace& w, hipStream_t s);
 hipError_t run_select(const Geometry& g, int layer, const float* p_raw, const float* p_ext,
                       const float* imp, uint64_t* bits, int32_t* idx, uint32_t* htop, char* ws,
                       const Workspace& w, hipStream_t s);

@@ -24,6 +24,12 @@
 // runs in the shadow of the score passes.  Per-layer scratch lives in a ring
 // of kRing slots.
 //
+// When the caller supplies the window rows' normalisers (the log-sum-exp its
+// prefill attention already computed for those query rows), pass 1 and the
+// lse stages drop out and the step takes L + 6 launches: pass 2 of the
+// last-O rows at j, their pool at j-1, pass 2 of the extended rows at j-2,
+// their pool at j-3, prep at j-4, select and count at j-5, gather at j-6.
+//
 // Work-group IDs are dispatched round-robin over the 8 XCDs, each with its
 // own L2.  Within a stage, consecutive tasks (e.g. the row tiles of one key
 // tile, which read the same K rows) are mapped to work-groups on the same
@@ -62,6 +68,8 @@ struct StepArgs {
   const char* k;
   const char* v;
   int64_t qs[4], ks[4], vs[4];
+  const float* lse;          // caller's natural-log row normalisers (else null)
+  int64_t ls[3];             // their strides {layer, batch, head}
   uint64_t* bits;
   int32_t* idx;
   int64_t idx_layer_stride;  // elements between layers of idx (0: one layer)
@@ -88,6 +96,9 @@ __device__ __forceinline__ ScoreIO score_io(const StepArgs& a, int layer, int sl
   io.psum_base = reinterpret_cast<float*>(sb + a.w.psum_base);
   io.psum_all = reinterpret_cast<float*>(sb + a.w.psum_all);
   io.ipart = reinterpret_cast<float*>(sb + a.w.ipart);
+  io.lse_in = a.lse ? a.lse + (int64_t)layer * a.ls[0] : nullptr;
+  io.lse_b = a.ls[1];
+  io.lse_h = a.ls[2];
   return io;
 }
 
@@ -430,6 +441,8 @@ void set_model(StepArgs& a, const ModelIO& m) {
     a.ks[i] = m.ks[i];
     a.vs[i] = m.vs[i];
   }
+  a.lse = m.lse;
+  for (int i = 0; i < 3; ++i) a.ls[i] = m.ls[i];
   a.bits = m.bits;
   a.idx = m.idx;
   a.k_out = static_cast<char*>(m.k_out);
@@ -460,10 +473,11 @@ hipError_t fill(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Pass 1, row normalisers and pass 2 of one layer into ring slot 0.
+// Pass 1, row normalisers and pass 2 of one layer into ring slot 0 (pass 2
+// alone when the caller gives the row normalisers).
 hipError_t score_stages(StepArgs a, const Workspace& w, hipStream_t s) {
   const int order[3] = {ST_PASS1, ST_LSE, ST_PASS2};
-  for (int i = 0; i < 3; ++i) {
+  for (int i = a.lse ? 2 : 0; i < 3; ++i) {
     for (int st = 0; st < ST_N; ++st) a.seg[st] = Seg{-1, 0, 0};
     a.seg[order[i]] = Seg{0, 0, seg_count(a.P, order[i])};
     const hipError_t e = launch(a, w, s);
@@ -491,6 +505,25 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
   a.idx_layer_stride = (int64_t)P.batch * P.H * P.B;
   a.out_layer = 1;
   a.standalone_counts = 0;
+  if (m.lse) {
+    // The row normalisers come from the caller (the log-sum-exp of the
+    // layer's prefill attention): no pass 1, a 6-launch pipeline.
+    const int n_launch = P.L + kPipeDepthLse;
+    for (int j = 0; j < n_launch; ++j) {
+      set_seg(a, ST_P2B, j);
+      set_seg(a, ST_POOLB, j - 1);
+      set_seg(a, ST_P2X, j - 2);
+      set_seg(a, ST_POOLX, j - 3);
+      set_seg(a, ST_PREP, j - 4);
+      set_seg(a, ST_SELECT, j - 5);
+      set_seg(a, ST_COUNT, j - 5);
+      set_seg(a, ST_GATHER, j - 6);
+      if (ev) (void)hipEventRecord(ev[j], s);
+      if ((e = launch(a, w, s)) != hipSuccess) return e;
+    }
+    if (ev) (void)hipEventRecord(ev[n_launch], s);
+    return hipSuccess;
+  }
   const int n_launch = P.L + kPipeDepth;
   for (int j = 0; j < n_launch; ++j) {
     set_seg(a, ST_P1B, j);
@@ -513,8 +546,8 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
 }
 
 hipError_t run_score(const Geometry& g, const void* q, const int64_t qs[3], const void* k,
-                     const int64_t ks[3], float* p_raw, float* p_ext, float* imp, char* ws,
-                     const Workspace& w, hipStream_t s) {
+                     const int64_t ks[3], const float* lse, const int64_t ls[2], float* p_raw,
+                     float* p_ext, float* imp, char* ws, const Workspace& w, hipStream_t s) {
   const Problem& P = g.p;
   hipError_t e = set_lds_limit(P, w);
   if (e != hipSuccess) return e;
@@ -524,6 +557,11 @@ hipError_t run_score(const Geometry& g, const void* q, const int64_t qs[3], cons
   for (int i = 0; i < 3; ++i) {
     a.qs[i + 1] = qs[i];
     a.ks[i + 1] = ks[i];
+  }
+  a.lse = lse;
+  if (lse) {
+    a.ls[1] = ls[0];
+    a.ls[2] = ls[1];
   }
   if ((e = score_stages(a, w, s)) != hipSuccess) return e;
   hipLaunchKernelGGL(finalize_kernel, dim3((P.Tc + 255) / 256, P.H + 1, P.batch), dim3(256), 0, s, P,

@@ -256,6 +256,8 @@ struct ScoreIO {
   int64_t ks_b, ks_h, ks_t;
   float2* lse_part;   // [b][HQ][Wn][n_kt1]
   float* lse2;        // [b][HQ][Wn]
+  const float* lse_in;  // nullable: caller's natural-log normalisers, rows contiguous
+  int64_t lse_b, lse_h;
   float* psum_base;   // [b][n_rt][H][Tc]
   float* psum_all;    // [b][n_rt][H][Tc]
   float* ipart;       // [b][n_rt][Tc]
@@ -386,8 +388,15 @@ struct ScoreTile {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int r = r_lo + rb * 16 + 4 * c + i;
-          const float v = io.lse2[((int64_t)b * P.HQ + j) * P.Wn + max(r, 0)];
-          nlse[bk][i] = (active && r >= 0) ? -v : -INFINITY;
+          // log2 of the row normaliser: from pass 1, or the caller's natural
+          // log times log2(e) (pass 2 works with base-2 exponentials)
+          const bool live = active && r >= 0;
+          float v = 0.f;
+          if (live)
+            v = io.lse_in ? io.lse_in[(int64_t)b * io.lse_b + (int64_t)j * io.lse_h + r] *
+                                1.4426950408889634f
+                          : io.lse2[((int64_t)b * P.HQ + j) * P.Wn + r];
+          nlse[bk][i] = live ? -v : -INFINITY;
         }
       }
       tile_base = active && r_lo + WR > base_lo;

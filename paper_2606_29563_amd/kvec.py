@@ -81,8 +81,9 @@ class Config:
 
 _lib = None
 
-EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_select_cover", "kvec_compact",
-           "kvec_evict_layer", "kvec_evict_model", "kvec_profile_points", "kvec_coverage",
+EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_score_lse", "kvec_select_cover",
+           "kvec_compact", "kvec_evict_layer", "kvec_evict_model", "kvec_evict_model_lse",
+           "kvec_profile_points", "kvec_profile_points_lse", "kvec_coverage",
            "kvec_status_string"]
 
 
@@ -100,19 +101,24 @@ def load() -> ctypes.CDLL:
     I64x = ctypes.POINTER(ctypes.c_int64)
     lib.kvec_workspace_size.argtypes = [P, ctypes.POINTER(sz)]
     lib.kvec_score.argtypes = [P, vp, I64x, vp, I64x, vp, vp, vp, vp, sz, vp]
+    lib.kvec_score_lse.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, sz, vp]
     lib.kvec_select_cover.argtypes = [P, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.kvec_compact.argtypes = [P, vp, I64x, vp, I64x, vp, vp, vp, vp]
     lib.kvec_evict_layer.argtypes = [P, i32, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp, sz, vp]
     lib.kvec_evict_model.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp, sz, vp,
                                      ctypes.POINTER(vp)]
+    lib.kvec_evict_model_lse.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp,
+                                         vp, sz, vp, ctypes.POINTER(vp)]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
     lib.kvec_profile_points.argtypes = [P]
+    lib.kvec_profile_points_lse.argtypes = [P]
     lib.kvec_status_string.argtypes = [ctypes.c_int]
     lib.kvec_status_string.restype = ctypes.c_char_p
     for name in EXPORTS:
-        if name not in ("kvec_status_string", "kvec_profile_points"):
+        if name not in ("kvec_status_string", "kvec_profile_points", "kvec_profile_points_lse"):
             getattr(lib, name).restype = ctypes.c_int
     lib.kvec_profile_points.restype = ctypes.c_int32
+    lib.kvec_profile_points_lse.restype = ctypes.c_int32
     _lib = lib
     return lib
 
@@ -139,6 +145,13 @@ def _strides(t, n: int):
     return (ctypes.c_int64 * n)(*st)
 
 
+def _lse_strides(t, n: int):
+    """Element strides of the leading n dims of an fp32 lse tensor with contiguous rows."""
+    import torch
+    assert t.dtype == torch.float32, "lse must be float32"
+    return _strides(t, n)
+
+
 def _stream(stream) -> int:
     import torch
     s = torch.cuda.current_stream() if stream is None else stream
@@ -158,6 +171,15 @@ def kvec_score(cfg: Config, q_win, k, p_raw, p_ext_raw, imp, ws, stream=None) ->
     _check(load().kvec_score(ctypes.byref(c), _ptr(q_win), _strides(q_win, 3), _ptr(k),
                              _strides(k, 3), _ptr(p_raw), _ptr(p_ext_raw), _ptr(imp), _ptr(ws),
                              ws.numel() * ws.element_size(), _stream(stream)), "kvec_score")
+
+
+def kvec_score_lse(cfg: Config, q_win, lse, k, p_raw, p_ext_raw, imp, ws, stream=None) -> None:
+    """As kvec_score, with the window rows' natural-log normalisers lse fp32 [b][HQ][O']."""
+    c = cfg.c()
+    _check(load().kvec_score_lse(ctypes.byref(c), _ptr(q_win), _strides(q_win, 3), _ptr(lse),
+                                 _lse_strides(lse, 2), _ptr(k), _strides(k, 3), _ptr(p_raw),
+                                 _ptr(p_ext_raw), _ptr(imp), _ptr(ws),
+                                 ws.numel() * ws.element_size(), _stream(stream)), "kvec_score_lse")
 
 
 def kvec_select_cover(cfg: Config, layer: int, p_raw, p_ext_raw, imp, cover_bits, idx,
@@ -198,6 +220,27 @@ def kvec_evict_model(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, ws
                                    _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream), ev),
            "kvec_evict_model")
+
+
+def kvec_evict_model_lse(cfg: Config, q_win, lse, k, v, cover_bits, idx, k_out, v_out, ws,
+                         stream=None, events=None) -> None:
+    """As kvec_evict_model, with the window rows' natural-log normalisers lse fp32
+    [L][b][HQ][O'] (events: kvec_profile_points_lse(cfg) handles)."""
+    c = cfg.c()
+    ev = None
+    if events is not None:
+        ev = (ctypes.c_void_p * len(events))(*events)
+    _check(load().kvec_evict_model_lse(ctypes.byref(c), _ptr(q_win), _strides(q_win, 4), _ptr(lse),
+                                       _lse_strides(lse, 3), _ptr(k), _strides(k, 4), _ptr(v),
+                                       _strides(v, 4), _ptr(cover_bits), _ptr(idx), _ptr(k_out),
+                                       _ptr(v_out), _ptr(ws), ws.numel() * ws.element_size(),
+                                       _stream(stream), ev),
+           "kvec_evict_model_lse")
+
+
+def kvec_profile_points_lse(cfg: Config) -> int:
+    c = cfg.c()
+    return int(load().kvec_profile_points_lse(ctypes.byref(c)))
 
 
 def kvec_profile_points(cfg: Config) -> int:

@@ -112,6 +112,30 @@ def test_entry_points_reject_before_launch():
     assert lib.kvec_coverage(ctypes.byref(c), fake, 32, fake, None) == kvec.KVEC_ERR_INVALID
     assert lib.kvec_compact(ctypes.byref(c), fake, ks3, None, ks3, fake, fake, fake,
                             None) == kvec.KVEC_ERR_INVALID
+    # caller-supplied row normalisers: null, misaligned, negative stride
+    ls2 = (ctypes.c_int64 * 2)(32 * 64, 64)
+    for lse, ls in ((None, ls2), (ctypes.c_void_p((1 << 20) + 2), ls2),
+                    (fake, (ctypes.c_int64 * 2)(-1, 64))):
+        assert lib.kvec_score_lse(ctypes.byref(c), fake, st3, lse, ls, fake, ks3, fake, fake, fake,
+                                  fake, 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    assert lib.kvec_score_lse(ctypes.byref(c), fake, st3, fake, ls2, fake, ks3, fake, fake, fake,
+                              fake, 16, None) == kvec.KVEC_ERR_WORKSPACE
+    st4 = (ctypes.c_int64 * 4)(32 * 64 * 128, 32 * 64 * 128, 64 * 128, 128)
+    ks4 = (ctypes.c_int64 * 4)(8 * 32768 * 128, 8 * 32768 * 128, 32768 * 128, 128)
+    ls3 = (ctypes.c_int64 * 3)(32 * 64, 32 * 64, 64)
+    assert lib.kvec_evict_model_lse(ctypes.byref(c), fake, st4, None, ls3, fake, ks4, fake, ks4,
+                                    fake, fake, fake, fake, fake, 1 << 40, None,
+                                    None) == kvec.KVEC_ERR_INVALID
+    assert lib.kvec_evict_model_lse(ctypes.byref(c), fake, st4, fake, ls3, fake, ks4, fake, ks4,
+                                    fake, fake, fake, fake, fake, 16, None,
+                                    None) == kvec.KVEC_ERR_WORKSPACE
+
+
+def test_profile_points():
+    assert kvec.kvec_profile_points(_cfg()) == 32 + 11
+    assert kvec.kvec_profile_points_lse(_cfg()) == 32 + 7
+    assert kvec.kvec_profile_points_lse(_cfg(seq_len=512, budget=1024)) == 0
+    assert kvec.kvec_profile_points_lse(_cfg(batch=0)) == -1
 
 
 def test_status_strings():

@@ -165,12 +165,25 @@ def test_compact_bit_exact(gpu_lib):
     np.testing.assert_array_equal(vo.cpu().view(torch.int16).numpy(), want_v)
 
 
-def _e2e(kv, w, check_layers=None):
-    """Run the whole-model driver and check sampled layers teacher-forced."""
+def oracle_lse_tensor(w):
+    """The oracle's window-row normalisers of every (layer, sequence), rounded to
+    fp32, on the device: [L][b][HQ][Wn] (what a prefill attention would hand over)."""
+    import torch
+    out = np.empty((w.n_layers, w.batch, w.n_q_heads, w.rows), dtype=np.float32)
+    for l in range(w.n_layers):
+        for b in range(w.batch):
+            out[l, b] = orc.to_f32(orc.window_lse(synth.to_f64(synth.queries(w, l, b), w.dtype),
+                                                  synth.to_f64(synth.keys(w, l, b), w.dtype)))
+    return torch.from_numpy(out).cuda()
+
+
+def _e2e(kv, w, check_layers=None, lse=False):
+    """Run the whole-model driver (kvec_evict_model, or kvec_evict_model_lse on
+    the oracle's row normalisers) and check sampled layers teacher-forced."""
     import torch
     cfg = kv.Config.from_workload(w)
     ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
-    _say(f"[e2e] {w.name}: generating inputs")
+    _say(f"[e2e] {w.name}{' (given lse)' if lse else ''}: generating inputs")
     q, k, v = model_tensors(w)
     L, H, B, T, d = w.n_layers, w.n_kv_heads, w.budget, w.seq_len, w.head_dim
     W = (T + 63) // 64
@@ -178,7 +191,10 @@ def _e2e(kv, w, check_layers=None):
     idx = torch.empty((L, w.batch, H, B), dtype=torch.int32, device="cuda")
     ko = torch.empty((L, w.batch, H, B, d), dtype=k.dtype, device="cuda")
     vo = torch.empty_like(ko)
-    kv.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
+    if lse:
+        kv.kvec_evict_model_lse(cfg, q, oracle_lse_tensor(w), k, v, bits, idx, ko, vo, ws)
+    else:
+        kv.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
     torch.cuda.synchronize()
     _say(f"[e2e] {w.name}: device step done")
     gi = idx.cpu().numpy()

@@ -121,6 +121,63 @@ def check_single_row_softmax(window_scores):
     np.testing.assert_allclose(pe[0], sm[:39], rtol=1e-13)
 
 
+def check_lse_constant_keys(window_lse):
+    """Every key of KV head h equal to c_h: every visible logit of row r of query
+    head j is s = q_{j,r} . c_{j//G} / sqrt(d), and row r at position p sees p+1
+    keys, so lse = s + ln(p + 1).  Distinct c_h pin the query-to-KV-head map."""
+    T, wn, hkv, g, d = 40, 6, 3, 2, 8
+    r = _rng(21)
+    c = r.standard_normal((hkv, d))
+    k = np.repeat(c[:, None, :], T, axis=1)
+    q = r.standard_normal((hkv * g, wn, d))
+    lse = window_lse(q, k)
+    assert lse.shape == (hkv * g, wn)
+    for j in range(hkv * g):
+        for row in range(wn):
+            s = float(q[j, row] @ c[j // g]) / math.sqrt(d)
+            want = s + math.log(T - wn + row + 1)
+            assert abs(lse[j, row] - want) <= 1e-12 * max(1.0, abs(want)), (j, row)
+
+
+def check_lse_brute(window_lse):
+    """Pure-Python loops, log of the fsum of exps over the causal keys."""
+    for seed, (T, wn, hkv, g, d) in enumerate([(15, 5, 2, 2, 4), (9, 9, 1, 3, 6)]):
+        r = _rng(300 + seed)
+        q = r.standard_normal((hkv * g, wn, d)) * 2.0
+        k = r.standard_normal((hkv, T, d)) * 2.0
+        lse = window_lse(q, k)
+        for j in range(hkv * g):
+            for row in range(wn):
+                p = T - wn + row
+                z = math.fsum(math.exp(math.fsum(q[j, row, i] * k[j // g, t, i] for i in range(d))
+                                       / math.sqrt(d)) for t in range(p + 1))
+                assert abs(lse[j, row] - math.log(z)) <= 1e-12 * max(1.0, abs(math.log(z)))
+
+
+def check_lse_normalises_scores(window_lse):
+    """One row, one head: exp(logit - lse) over the candidates is the score P of
+    window_scores (O = O' = 1), which the mass identity pins independently."""
+    r = _rng(22)
+    q = r.standard_normal((1, 1, 8)) * 3
+    k = r.standard_normal((1, 50, 8))
+    lse = window_lse(q, k)
+    p, _, _ = orc.window_scores(q, k, 1)
+    s = (k[0, :49] @ q[0, 0]) / math.sqrt(8)
+    np.testing.assert_allclose(np.exp(s - lse[0, 0]), p[0], rtol=1e-12)
+
+
+def test_lse_constant_keys():
+    check_lse_constant_keys(orc.window_lse)
+
+
+def test_lse_brute_force():
+    check_lse_brute(orc.window_lse)
+
+
+def test_lse_normalises_scores():
+    check_lse_normalises_scores(orc.window_lse)
+
+
 def test_zero_query_closed_form():
     check_zero_query_closed_form(orc.window_scores)
 
@@ -471,6 +528,31 @@ def _mut_query_head_max(q_win, k, window, full=False):
     return p[:, :tc], pe[:, :tc], imp[:tc]
 
 
+def _mut_lse_no_causal(q_win, k):
+    hq, wn, d = q_win.shape
+    g = hq // k.shape[0]
+    out = np.zeros((hq, wn))
+    for j in range(hq):
+        s = (q_win[j] @ k[j // g].T) / math.sqrt(d)          # mistake: every key visible
+        m = s.max(axis=1)
+        out[j] = m + np.log(np.exp(s - m[:, None]).sum(axis=1))
+    return out
+
+
+def _mut_lse_head_map(q_win, k):
+    hq = q_win.shape[0]
+    hkv = k.shape[0]
+    out = np.zeros(q_win.shape[:2])
+    for j in range(hq):                                       # mistake: j % H_kv, not j // G
+        out[j] = orc.window_lse(q_win[j:j + 1], k[j % hkv:j % hkv + 1])[0]
+    return out
+
+
+def _mut_lse_no_scale(q_win, k):
+    d = q_win.shape[2]
+    return orc.window_lse(q_win * math.sqrt(d), k)            # mistake: scale 1/sqrt(d) dropped
+
+
 def _mut_highest_sigma(sigma, delta):
     order = sorted(range(len(sigma)), key=lambda h: (-float(sigma[h]), h))   # mistake
     return np.array(sorted(order[:delta]), dtype=np.int64)
@@ -521,6 +603,11 @@ def _mut_preserve_raw(p_raw, p_ext_raw, imp, n_t, layer, **kw):
     (check_zero_query_closed_form, _mut_wrong_window),
     (check_brute_force, _mut_no_causal),
     (check_brute_force, _mut_query_head_max),
+    (check_lse_constant_keys, _mut_lse_no_causal),
+    (check_lse_constant_keys, _mut_lse_head_map),
+    (check_lse_constant_keys, _mut_lse_no_scale),
+    (check_lse_brute, _mut_lse_no_causal),
+    (check_lse_normalises_scores, _mut_lse_no_scale),
     (check_lowest_sigma, _mut_highest_sigma),
     (check_bonus_hand, _mut_layer_denominator),
     (check_sigma, _mut_sample_std),
