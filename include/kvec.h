@@ -81,7 +81,7 @@ typedef struct kvec_config {
   int32_t batch;          /* independent sequences, >= 1 */
   int32_t n_layers;       /* L, >= 1 (rows of the coverage bitmap) */
   int32_t n_kv_heads;     /* H in {1, 2, 4, 8} */
-  int32_t n_q_heads;      /* multiple of H; G = n_q_heads / H in {1, 2, 4, 8} */
+  int32_t n_q_heads;      /* multiple of H; G = n_q_heads / H in 1..8 */
   int32_t head_dim;       /* d in {64, 128} */
   int32_t seq_len;        /* T, prefix length including the window, 1..262144 */
   int32_t window;         /* O, 1 <= O <= T */

@@ -13,7 +13,11 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkvec.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["kvec_api.hip", "kvec_pipeline.hip"]
+# (source, object name, extra flags): the step kernel is instantiated once per
+# (dtype, head_dim) pair, in parallel translation units
+SOURCES = [("kvec_api.hip", "kvec_api", []), ("kvec_pipeline.hip", "kvec_pipeline", [])] + [
+    ("kvec_step_inst.hip", f"kvec_step_{tt.lower()}_d{d}", [f"-DKVEC_INST_TT={tt}", f"-DKVEC_INST_D={d}"])
+    for tt in ("BF16", "F32") for d in (64, 128)]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -24,9 +28,10 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(item) -> str:
+    src, name, extra = item
+    obj = os.path.join(BUILD_DIR, name + ".o")
+    cmd = [HIPCC, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
@@ -35,7 +40,8 @@ def _compile(src: str) -> str:
 
 def build(verbose: bool = True) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+    workers = max(1, min(len(SOURCES), int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
+    with cf.ThreadPoolExecutor(max_workers=workers) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp],

@@ -29,7 +29,7 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   if (c->head_dim < 1) return KVEC_ERR_INVALID;
   const int H = c->n_kv_heads, G = c->n_q_heads / c->n_kv_heads;
   if (H != 1 && H != 2 && H != 4 && H != 8) return KVEC_ERR_UNSUPPORTED;
-  if (G != 1 && G != 2 && G != 4 && G != 8) return KVEC_ERR_UNSUPPORTED;
+  if (G < 1 || G > 8) return KVEC_ERR_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return KVEC_ERR_UNSUPPORTED;
   if (c->seq_len > (1 << 18)) return KVEC_ERR_UNSUPPORTED;
   if (c->pool_kernel > 63) return KVEC_ERR_UNSUPPORTED;

@@ -36,289 +36,12 @@
 // XCD so that K is fetched once per XCD L2.
 #include <string.h>
 
-#include "kvec_score_dev.h"
-#include "kvec_select_dev.h"
+#include "kvec_step.h"
 
 namespace kvec {
 namespace {
 
-// Segments are dispatched in this order (long work-groups first).  *_B and
-// *_X are the last-O and the extended-window halves of the layer pipeline;
-// the plain stages cover every row and head (per-layer entry points).
-enum Stage {
-  ST_SELECT = 0, ST_COUNT,
-  ST_PASS2, ST_P2B, ST_P2X,
-  ST_PASS1, ST_P1B, ST_P1X,
-  ST_LSE, ST_LSEB, ST_LSEX,
-  ST_POOL, ST_POOLB, ST_POOLX,
-  ST_PREP, ST_GATHER, ST_N
-};
-
-struct Seg {
-  int layer;  // model layer the stage works on
-  int slot;   // ring slot of that layer's scratch
-  int count;  // tasks of this stage in the launch (work-groups: rounded up to 8)
-};
-
-struct StepArgs {
-  Problem P;
-  Workspace w;
-  char* ws;
-  const char* q;
-  const char* k;
-  const char* v;
-  int64_t qs[4], ks[4], vs[4];
-  const float* lse;          // caller's natural-log row normalisers (else null)
-  int64_t ls[3];             // their strides {layer, batch, head}
-  uint64_t* bits;
-  int32_t* idx;
-  int64_t idx_layer_stride;  // elements between layers of idx (0: one layer)
-  char* k_out;
-  char* v_out;
-  int out_layer;             // 1: k_out/v_out have a layer dimension
-  const float* p_raw;        // standalone selection inputs (else null)
-  const float* p_ext;
-  const float* imp_in;
-  uint32_t* htop;
-  int standalone_counts;     // selection reads complete n_t from the counts buffer
-  Seg seg[ST_N];
-};
-
-__device__ __forceinline__ ScoreIO score_io(const StepArgs& a, int layer, int slot) {
-  ScoreIO io;
-  char* sb = a.ws + (size_t)slot * a.w.slot_bytes;
-  io.q = a.q + (int64_t)layer * a.qs[0] * a.P.esize;
-  io.k = a.k + (int64_t)layer * a.ks[0] * a.P.esize;
-  io.qs_b = a.qs[1]; io.qs_h = a.qs[2]; io.qs_r = a.qs[3];
-  io.ks_b = a.ks[1]; io.ks_h = a.ks[2]; io.ks_t = a.ks[3];
-  io.lse_part = reinterpret_cast<float2*>(sb + a.w.lse_part);
-  io.lse2 = reinterpret_cast<float*>(sb + a.w.lse2);
-  io.psum_base = reinterpret_cast<float*>(sb + a.w.psum_base);
-  io.psum_all = reinterpret_cast<float*>(sb + a.w.psum_all);
-  io.ipart = reinterpret_cast<float*>(sb + a.w.ipart);
-  io.lse_in = a.lse ? a.lse + (int64_t)layer * a.ls[0] : nullptr;
-  io.lse_b = a.ls[1];
-  io.lse_h = a.ls[2];
-  return io;
-}
-
-__device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int slot) {
-  SelectIO io;
-  char* sb = a.ws + (size_t)slot * a.w.slot_bytes;
-  const bool standalone = a.p_raw != nullptr;
-  io.psum_base = standalone ? nullptr : reinterpret_cast<const float*>(sb + a.w.psum_base);
-  io.psum_all = standalone ? nullptr : reinterpret_cast<const float*>(sb + a.w.psum_all);
-  io.ipart = reinterpret_cast<const float*>(sb + a.w.ipart);
-  io.p_raw = a.p_raw;
-  io.p_ext = a.p_ext;
-  io.imp_in = a.imp_in;
-  io.imp = standalone ? const_cast<float*>(a.imp_in) : reinterpret_cast<float*>(sb + a.w.imp);
-  io.pooled = reinterpret_cast<float*>(sb + a.w.pooled);
-  io.pooled_ext = reinterpret_cast<float*>(sb + a.w.pooled_ext);
-  io.stats = reinterpret_cast<double2*>(sb + a.w.stats);
-  io.hist = reinterpret_cast<uint32_t*>(sb + a.w.hist);
-  io.mem_t = reinterpret_cast<int32_t*>(sb + a.w.mem_t);
-  io.mem_ps = reinterpret_cast<float*>(sb + a.w.mem_ps);
-  io.mem_i = reinterpret_cast<float*>(sb + a.w.mem_i);
-  io.mem_n = reinterpret_cast<int32_t*>(sb + a.w.mem_n);
-  io.htop_mask = a.htop;
-  io.spill_keys = reinterpret_cast<uint32_t*>(a.ws + a.w.spill);
-  io.spill_t = reinterpret_cast<int32_t*>(a.ws + a.w.spill + a.w.spill_stride);
-  io.spill_ps = reinterpret_cast<float*>(a.ws + a.w.spill + 2 * a.w.spill_stride);
-  io.spill_i = reinterpret_cast<float*>(a.ws + a.w.spill + 3 * a.w.spill_stride);
-  const uint8_t* cnt = reinterpret_cast<const uint8_t*>(a.ws + a.w.counts);
-  if (a.standalone_counts) {
-    // counts of the caller's earlier rows, computed for this call
-    io.cnt_in = cnt;
-    io.bits_prev = nullptr;
-  } else {
-    // pipeline: n_t(l) = counts(l-1) + kept bit of layer l-1
-    io.cnt_in = layer >= 2 ? cnt + (size_t)((layer - 1) & 1) * a.w.counts_stride : nullptr;
-    io.bits_prev = layer >= 1 ? a.bits + (int64_t)(layer - 1) * a.P.words : nullptr;
-  }
-  io.bits = a.bits;
-  io.idx = a.idx + (int64_t)layer * a.idx_layer_stride;
-  return io;
-}
-
-// Cache store (Sec. 4.1): out[b][h][i] = K[b][h][idx[b][h][i]] (and V),
-// one 16-byte chunk per thread and round, 4 rounds per work-group; idx
-// outside [0, T) -> zeros.  All index loads are issued first, then all row
-// loads, then the stores (one memory round trip each).
-__device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b, int part) {
-  constexpr int kRounds = 4;
-  const Problem& P = a.P;
-  const int cpr = P.D * P.esize / 16;
-  const int64_t total = (int64_t)P.H * P.B * cpr;
-  const int32_t* idx = a.idx + (int64_t)layer * a.idx_layer_stride + (int64_t)b * P.H * P.B;
-  const int64_t orow0 = ((int64_t)(a.out_layer ? layer : 0) * P.batch + b) * P.H * P.B;
-  int64_t ci[kRounds];
-  int id[kRounds];
-#pragma unroll
-  for (int e = 0; e < kRounds; ++e) {
-    ci[e] = ((int64_t)part * kRounds + e) * kThreads + threadIdx.x;
-    id[e] = ci[e] < total ? idx[ci[e] / cpr] : -1;
-  }
-  uint4 kv[kRounds], vv[kRounds];
-#pragma unroll
-  for (int e = 0; e < kRounds; ++e) {
-    kv[e] = make_uint4(0, 0, 0, 0);
-    vv[e] = make_uint4(0, 0, 0, 0);
-    if (ci[e] < total && id[e] >= 0 && id[e] < P.T) {
-      const int ch = (int)(ci[e] % cpr);
-      const int h = (int)((ci[e] / cpr) / P.B);
-      const int64_t ko = ((int64_t)layer * a.ks[0] + (int64_t)b * a.ks[1] + (int64_t)h * a.ks[2] +
-                          (int64_t)id[e] * a.ks[3]) * P.esize;
-      const int64_t vo = ((int64_t)layer * a.vs[0] + (int64_t)b * a.vs[1] + (int64_t)h * a.vs[2] +
-                          (int64_t)id[e] * a.vs[3]) * P.esize;
-      kv[e] = reinterpret_cast<const uint4*>(a.k + ko)[ch];
-      vv[e] = reinterpret_cast<const uint4*>(a.v + vo)[ch];
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < kRounds; ++e) {
-    if (ci[e] < total) {
-      const int64_t o = (orow0 + ci[e] / cpr) * cpr + ci[e] % cpr;
-      reinterpret_cast<uint4*>(a.k_out)[o] = kv[e];
-      reinterpret_cast<uint4*>(a.v_out)[o] = vv[e];
-    }
-  }
-}
-
-// First window row held by the row tiles of the last-O rows.
-__host__ __device__ inline int base_row_lo(const Problem& P) { return max(0, P.Wn - P.n_rt_base * P.WR); }
-
-// Row-normaliser tasks per sequence of one LSE stage.
-__host__ __device__ inline int lse_tasks_per_seq(const Problem& P, int st) {
-  const int rb0 = base_row_lo(P);
-  const int nr = st == ST_LSEB ? P.Wn - rb0 : st == ST_LSEX ? rb0 : P.Wn;
-  return (P.HQ * nr + kLseRows - 1) / kLseRows;
-}
-
-template <class TT, int D, int G>
-__global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
-  extern __shared__ __align__(16) char smem[];
-  const Problem P = a.P;
-  int blk = blockIdx.x;
-  int st = 0;
-  for (; st < ST_N; ++st) {
-    const int n8 = (a.seg[st].count + 7) & ~7;
-    if (blk < n8) break;
-    blk -= n8;
-  }
-  if (st >= ST_N) return;
-  const Seg sg = a.seg[st];
-  {
-    // XCD-aware remap: segments start at multiples of 8, so blk % 8 is the XCD
-    const int n8 = (sg.count + 7) & ~7;
-    blk = (blk & 7) * (n8 >> 3) + (blk >> 3);
-    if (blk >= sg.count) return;
-  }
-  switch (st) {
-    case ST_SELECT: {
-      const int b = blk / P.H, h = blk % P.H;
-      task_select(P, select_io(a, sg.layer, sg.slot), sg.layer, b, h, smem);
-      break;
-    }
-    case ST_COUNT: {
-      const int parts = (P.words + kCountWords - 1) / kCountWords;
-      const int b = blk / parts;
-      const int layer = sg.layer;
-      const uint8_t* cbase = reinterpret_cast<const uint8_t*>(a.ws + a.w.counts);
-      const uint8_t* prev = layer >= 2 ? cbase + (size_t)((layer - 1) & 1) * a.w.counts_stride : nullptr;
-      const uint64_t* row = layer >= 1 ? a.bits + (int64_t)(layer - 1) * P.words : nullptr;
-      uint8_t* out = reinterpret_cast<uint8_t*>(a.ws + a.w.counts) + (size_t)(layer & 1) * a.w.counts_stride;
-      task_count(P, prev, row, out, b, blk % parts);
-      break;
-    }
-    case ST_PASS1:
-    case ST_P1B:
-    case ST_P1X: {
-      const Part part = st == ST_P1B ? PART_BASE : st == ST_P1X ? PART_EXT : PART_ALL;
-      const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
-      const int per_b = P.n_kt1 * n_rtg;
-      const int b = blk / per_b, rem = blk % per_b;
-      const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b) : 0u;
-      score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot), b, rem / n_rtg, rem % n_rtg,
-                              reinterpret_cast<float*>(smem), part, hm);
-      break;
-    }
-    case ST_LSE:
-    case ST_LSEB:
-    case ST_LSEX: {
-      const int per_b = lse_tasks_per_seq(P, st);
-      const int b = blk / per_b;
-      const int rb0 = base_row_lo(P);
-      const uint32_t all = (1u << P.H) - 1u;
-      const ScoreIO io = score_io(a, sg.layer, sg.slot);
-      if (st == ST_LSE)
-        task_lse<TT, D, G>(P, io, b, blk % per_b, 0, P.Wn, all);
-      else if (st == ST_LSEB)
-        task_lse<TT, D, G>(P, io, b, blk % per_b, rb0, P.Wn - rb0, all);
-      else
-        task_lse<TT, D, G>(P, io, b, blk % per_b, 0, rb0,
-                           htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b));
-      break;
-    }
-    case ST_PASS2:
-    case ST_P2B:
-    case ST_P2X: {
-      const Part part = st == ST_P2B ? PART_BASE : st == ST_P2X ? PART_EXT : PART_ALL;
-      const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
-      const int per_b = P.n_kt2 * n_rtg;
-      const int b = blk / per_b, rem = blk % per_b;
-      const ScoreIO io = score_io(a, sg.layer, sg.slot);
-      const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b) : 0u;
-      score_tile<TT, D, G, 2>(P, io, b, rem / n_rtg, rem % n_rtg, reinterpret_cast<float*>(smem),
-                              part, hm);
-      if (part != PART_EXT) {
-        // Clear this sequence's histograms for the pool stages of this layer.
-        uint32_t* hist = reinterpret_cast<uint32_t*>(a.ws + (size_t)sg.slot * a.w.slot_bytes + a.w.hist) +
-                         (int64_t)b * 2 * P.H * kHistBins;
-        const int nwords = 2 * P.H * kHistBins;
-        const int per = (nwords + per_b - 1) / per_b;
-        for (int i = rem * per + threadIdx.x; i < min(nwords, (rem + 1) * per); i += kThreads) hist[i] = 0u;
-      }
-      break;
-    }
-    case ST_PREP: {
-      const int nt = (P.n_prep + kPrepPer - 1) / kPrepPer;
-      const int per_b = P.H * nt;
-      const int b = blk / per_b, rem = blk % per_b;
-      const int c0 = (rem % nt) * kPrepPer;
-      task_prep(P, select_io(a, sg.layer, sg.slot), sg.layer, b, rem / nt, c0,
-                min(P.n_prep, c0 + kPrepPer), smem);
-      break;
-    }
-    case ST_POOL:
-    case ST_POOLB: {
-      const int nt = (P.n_pool + kPoolPer - 1) / kPoolPer;
-      const int per_b = P.H * nt;
-      const int b = blk / per_b, rem = blk % per_b;
-      const int c0 = (rem % nt) * kPoolPer;
-      task_pool(P, select_io(a, sg.layer, sg.slot), b, rem / nt, c0, min(P.n_pool, c0 + kPoolPer),
-                smem, true, st == ST_POOL);
-      break;
-    }
-    case ST_POOLX: {
-      const int nt = (P.n_pool + kPoolPer - 1) / kPoolPer;
-      const int per_b = P.delta_eff * nt;
-      const int b = blk / per_b, rem = blk % per_b;
-      const SelectIO io = select_io(a, sg.layer, sg.slot);
-      const int h = nth_bit(htop_mask(P, io.stats, b), rem / nt);
-      const int c0 = (rem % nt) * kPoolPer;
-      if (h >= 0) task_pool(P, io, b, h, c0, min(P.n_pool, c0 + kPoolPer), smem, false, true);
-      break;
-    }
-    case ST_GATHER: {
-      const int b = blk / P.n_gather;
-      task_gather(a, sg.layer, b, blk % P.n_gather);
-      break;
-    }
-  }
-}
+using namespace step;
 
 __global__ void fill_u32_kernel(uint32_t* p, int64_t n, uint32_t v) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -403,18 +126,6 @@ int seg_count(const Problem& P, int st) {
     case ST_GATHER: return P.batch * P.n_gather;
   }
   return 0;
-}
-
-typedef void (*StepFn)(StepArgs);
-
-template <class TT, int D>
-StepFn pick_g(int G) {
-  switch (G) {
-    case 1: return step_kernel<TT, D, 1>;
-    case 2: return step_kernel<TT, D, 2>;
-    case 4: return step_kernel<TT, D, 4>;
-    default: return step_kernel<TT, D, 8>;
-  }
 }
 
 StepFn pick(const Problem& P) {

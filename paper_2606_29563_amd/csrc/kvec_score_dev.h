@@ -298,6 +298,7 @@ template <class TT, int D, int G, int PASS>
 struct ScoreTile {
   using Tl = Tiling<G>;
   static constexpr int RB = Tl::RB, NB = Tl::NB, WR = Tl::WR;
+  static constexpr int NBP = (NB + 3) & ~3;  // blocks padded to groups of four (pass-1 store)
   static constexpr int ES = elem_bytes<TT>();
 
   const Problem& P;
@@ -318,8 +319,8 @@ struct ScoreTile {
   int kstride;                    // bytes between consecutive keys
   int voff[KR::NI];               // byte offset of this lane's piece in each load
   f32x4 acc[NB];
-  float mref[NB];  // pass 1: wave-uniform reference of each block
-  float lsum[NB][4], nlse[NB][4];
+  float mref[NBP];  // pass 1: wave-uniform reference of each block
+  float lsum[NBP][4], nlse[NB][4];
   int pos[RB][4];
 
   // part: which row tiles and heads (PART_EXT: the heads set in hmask).
@@ -377,9 +378,11 @@ struct ScoreTile {
     tile_base = tile_mixed = wg_base = false;
     if constexpr (PASS == 1) {
 #pragma unroll
-      for (int bk = 0; bk < NB; ++bk)
+      for (int bk = 0; bk < NBP; ++bk) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) lsum[bk][i] = 0.f;
+        if (bk >= NB) mref[bk] = 0.f;  // padding blocks are never stored
+      }
     } else {
 #pragma unroll
       for (int bk = 0; bk < NB; ++bk) {
@@ -737,7 +740,7 @@ struct ScoreTile {
     const float m = has_keys ? mb : -INFINITY;
     if (!has_keys) l = 0.f;
     else if (!(l >= 0x1p-64f && l < INFINITY)) l = INFINITY;  // exact recompute
-    if (active && r >= 0)
+    if (active && r >= 0 && bk < NB)
       io.lse_part[(((int64_t)b * P.HQ + j) * P.Wn + r) * P.n_kt1 + kt] = make_float2(m, l);
   }
 
@@ -763,9 +766,9 @@ struct ScoreTile {
     } else {
       // Row sums of 4 blocks (16 quantities: block, row of the lane group) at a
       // time; lane n of each row ends with quantity n and stores its partial.
-      static_assert(NB == 4 || NB == 8, "blocks in groups of four");
+      static_assert(NBP == 4 || NBP == 8, "blocks in groups of four");
       store_partials<0>();
-      if constexpr (NB == 8) store_partials<4>();
+      if constexpr (NBP == 8) store_partials<4>();
     }
   }
 };

@@ -121,7 +121,7 @@ def _hh(frac: float, T: int) -> int:
     return int(round(frac * T))
 
 
-# The five measured workloads.  Heavy-hitter counts are fractions of the prefix
+# The measured workloads.  Heavy-hitter counts are fractions of the prefix
 # length T: 2% (tiny, 4k), 1% (32k), 2% with an 80% shared core (16k x 8),
 # 0.5% from a Zipf(1.1) over 256 clusters (128k).
 WORKLOADS = {
@@ -135,6 +135,10 @@ WORKLOADS = {
                 hh_count=_hh(0.02, 16384), hh_shared=int(0.8 * _hh(0.02, 16384))),
     4: Workload("llama8b-128k", 32, 8, 32, 128, 131072, 1, 32, 64, 2048, 7, "bf16", 1004,
                 hh_count=_hh(0.005, 131072), zipf_clusters=256),
+    # The paper's second model (Qwen2.5-7B-Instruct, Sec. 5.3): 28 layers, 4 KV
+    # and 28 query heads (GQA group 7), d = 128, RoPE theta 1e6; the 32k recipe.
+    5: Workload("qwen7b-32k", 28, 4, 28, 128, 32768, 1, 32, 64, 1024, 7, "bf16", 1005,
+                rope_theta=1000000.0, hh_count=_hh(0.01, 32768), sink_count=64),
 }
 
 

@@ -72,7 +72,7 @@ def test_workspace_size_positive_and_monotone():
     (dict(beta=1.5), kvec.KVEC_ERR_INVALID),
     (dict(dtype=7), kvec.KVEC_ERR_INVALID),
     (dict(head_dim=96), kvec.KVEC_ERR_UNSUPPORTED),
-    (dict(n_q_heads=24), kvec.KVEC_ERR_UNSUPPORTED),        # G = 3
+    (dict(n_q_heads=72), kvec.KVEC_ERR_UNSUPPORTED),        # G = 9
     (dict(n_kv_heads=16, n_q_heads=32), kvec.KVEC_ERR_UNSUPPORTED),
     (dict(n_kv_heads=3, n_q_heads=12), kvec.KVEC_ERR_UNSUPPORTED),
     (dict(seq_len=300000), kvec.KVEC_ERR_UNSUPPORTED),

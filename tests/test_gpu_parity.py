@@ -41,6 +41,11 @@ SCORE_CASES = [
     _small("bf16-d64-g2-short", 70, 16, 64, 2, 2, 64, "bf16"),
     _small("f32-d128-g1", 200, 8, 8, 2, 1, 128, "f32"),
     _small("bf16-d128-g4-wn-eq-o", 600, 32, 32, 4, 4, 128, "bf16"),
+    # group sizes that are not powers of two (Qwen2.5: 7 for 7B, 5 for 14B/32B, 6 for 1.5B)
+    _small("bf16-d128-g7-h4", 1500, 32, 64, 4, 7, 128, "bf16"),
+    _small("bf16-d64-g3-ragged", 611, 12, 24, 2, 3, 64, "bf16"),
+    _small("bf16-d128-g5-h8", 800, 16, 32, 8, 5, 128, "bf16"),
+    _small("f32-d128-g6-h2", 500, 20, 40, 2, 6, 128, "f32"),
 ]
 
 
@@ -244,6 +249,10 @@ def test_e2e_small_bf16(gpu_lib):
     _e2e(gpu_lib, _small("e2e-small", 2500, 32, 64, 8, 4, 128, "bf16", B=200, layers=6))
 
 
+def test_e2e_group7_bf16(gpu_lib):
+    _e2e(gpu_lib, _small("e2e-g7", 3000, 32, 64, 4, 7, 128, "bf16", B=256, layers=4))
+
+
 def test_layer_calls_match_model_step(gpu_lib):
     """kvec_evict_layer called layer by layer reproduces kvec_evict_model exactly."""
     import torch
@@ -295,7 +304,12 @@ def test_full_llama8b_128k_sampled_layers(gpu_lib):
     _e2e(gpu_lib, synth.workload(4), check_layers=[0, 31])
 
 
-@pytest.mark.parametrize("wi", [2, 3, 4], ids=["32k", "16k-b8", "128k"])
+def test_full_qwen7b_32k_sampled_layers(gpu_lib):
+    """The Qwen2.5-7B shape (4 KV / 28 query heads, 28 layers) at 32k."""
+    _e2e(gpu_lib, synth.workload(5), check_layers=[0, 1, 27])
+
+
+@pytest.mark.parametrize("wi", [2, 3, 4, 5], ids=["32k", "16k-b8", "128k", "qwen7b-32k"])
 def test_full_size_scores(gpu_lib, wi):
     """kvec_score on one layer of a full-size shape against the oracle scores."""
     import torch
