@@ -312,7 +312,7 @@ def main():
         "config": {"workload": w.name, "layers": L, "batch": b, "kv_heads": H, "q_heads": HQ,
                    "head_dim": d, "seq_len": T, "window": w.window, "window_ext": w.window_ext,
                    "budget": B, "pool": w.pool_kernel, "delta": w.n_adjust_heads,
-                   "lambda": w.lam, "beta": w.beta},
+                   "lambda": w.lam, "beta": w.beta, "head_criterion": w.criterion},
         "roofline": roof,
         "cpu_baseline": cpu,
     }

@@ -71,6 +71,14 @@ typedef enum kvec_status {
   KVEC_ERR_DEVICE = 4        /* a HIP launch or runtime call failed */
 } kvec_status;
 
+/* How H_top picks the heads that are rescored over O' (Sec. 4.1). */
+typedef enum kvec_head_criterion {
+  KVEC_HEADS_STD = 0,     /* the delta heads with the lowest std of pooled P (Sec. 4.1) */
+  KVEC_HEADS_ENTROPY = 1  /* the delta heads with the highest entropy of pooled P taken as a
+                             distribution over the candidates (the alternative criterion of
+                             the head-selection ablation, Sec. 5.4) */
+} kvec_head_criterion;
+
 typedef enum kvec_dtype {
   KVEC_BF16 = 0,  /* Q, K, V and the compacted cache are bfloat16 */
   KVEC_F32 = 1    /* ... are IEEE float32 */
@@ -92,6 +100,7 @@ typedef struct kvec_config {
   float lambda;           /* >= 0: cross-layer bonus weight (0 = off) */
   float beta;             /* in [0, 1]: preserve K = min(floor(beta*B), B-O) per head */
   int32_t dtype;          /* kvec_dtype of Q, K, V and the compacted cache */
+  int32_t head_criterion; /* kvec_head_criterion of H_top (KVEC_HEADS_STD is the paper's) */
 } kvec_config;
 
 /* Bytes of workspace the score/select/evict calls need for `cfg`.
@@ -134,6 +143,8 @@ kvec_status kvec_score_lse(const kvec_config* cfg,
                            void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Selection of one layer from its scores (Algorithm 1, then top-B, Sec. 4.1-4.2).
+ * H_top follows cfg->head_criterion; sigma and the entropy are float64 sums
+ * over the pooled P of the candidates.
  *   layer       0-based index l; coverage uses n_t/(l+1).
  *   p_raw, p_ext_raw, imp  device fp32, as written by kvec_score.
  *   cover_bits  device uint64 [batch][n_layers][ceil(T/64)]: bit (l', t) set

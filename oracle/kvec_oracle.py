@@ -14,6 +14,7 @@ of LLM" (K-VEC).  Each function names the passage it follows:
 * head focus sigma = std of P over tokens         Sec. 4.1
 * H_top = delta heads with the LOWEST sigma,
   their P recomputed over the extended window O'  Sec. 4.1; Algorithm 1
+* alternative head criterion: entropy             Sec. 5.4 (head-selection ablation)
 * coverage = n_t / (l + 1)                        Sec. 4.2
 * global importance I = mean over the window of
   the max over heads of A                         Sec. 4.2
@@ -44,6 +45,7 @@ import numpy as np
 
 __all__ = [
     "window_attention", "window_lse", "window_scores", "to_f32", "maxpool1d", "head_sigma",
+    "head_entropy", "focus_heads",
     "adjusted_heads", "rank_first", "preserve_count", "adjusted_priority",
     "LayerResult", "select_layer", "evict_layer_from_scores", "score_layer",
     "gather_rows", "coverage_count", "counts_from_bits", "layer_bits",
@@ -165,6 +167,31 @@ def head_sigma(p: np.ndarray) -> np.ndarray:
     return np.sqrt(((x - mean[:, None]) ** 2).sum(axis=1) / x.shape[1])
 
 
+def head_entropy(p: np.ndarray) -> np.ndarray:
+    """Shannon entropy (natural log) of each head's scores taken as a distribution
+    over tokens, in float64: H_h = -sum_t q_t ln q_t with q_t = P[h,t] / sum_u P[h,u]
+    (0 ln 0 = 0; a head whose scores are all zero has entropy 0)."""
+    x = np.asarray(p, dtype=np.float64)
+    out = np.zeros(x.shape[0])
+    for h in range(x.shape[0]):
+        tot = x[h].sum()
+        if tot > 0:
+            q = x[h][x[h] > 0] / tot
+            out[h] = -(q * np.log(q)).sum()
+    return out
+
+
+def focus_heads(pooled: np.ndarray, delta: int, criterion: str = "std") -> np.ndarray:
+    """H_top by the paper's criterion (the delta lowest sigma, Sec. 4.1) or by the
+    alternative of the head-selection ablation (Sec. 5.4): the delta least focused
+    heads by entropy, i.e. the highest entropy.  Ties: lower head index first."""
+    if criterion == "std":
+        return adjusted_heads(head_sigma(pooled), delta)
+    if criterion == "entropy":
+        return adjusted_heads(-head_entropy(pooled), delta)
+    raise ValueError(criterion)
+
+
 def adjusted_heads(sigma: np.ndarray, delta: int) -> np.ndarray:
     """H_top: the delta heads with the lowest sigma (ties: lower head index first)."""
     order = sorted(range(len(sigma)), key=lambda h: (float(sigma[h]), h))
@@ -225,7 +252,8 @@ class LayerResult:
 
 def select_layer(p_raw: np.ndarray, p_ext_raw: np.ndarray, imp: np.ndarray, n_t: np.ndarray,
                  layer: int, *, T: int, window: int, window_ext: int, budget: int,
-                 pool_kernel: int, delta: int, lam: float, beta: float) -> LayerResult:
+                 pool_kernel: int, delta: int, lam: float, beta: float,
+                 criterion: str = "std") -> LayerResult:
     """The per-layer K-VEC policy on fp32 scores (Algorithm 1, then top-B and the window).
 
     p_raw, p_ext_raw: [H][Tc] fp32; imp: [Tc] fp32; n_t: [T] (or [Tc]) layer counts."""
@@ -243,7 +271,7 @@ def select_layer(p_raw: np.ndarray, p_ext_raw: np.ndarray, imp: np.ndarray, n_t:
     pooled_ext = maxpool1d(p_ext_raw.astype(np.float32), pool_kernel)
     sigma = head_sigma(pooled)
     wn = min(window_ext, T)
-    htop = adjusted_heads(sigma, delta) if wn > O else np.zeros(0, np.int64)
+    htop = focus_heads(pooled, delta, criterion) if wn > O else np.zeros(0, np.int64)
     p_sel = pooled.copy()
     p_sel[htop] = pooled_ext[htop]
     kp = preserve_count(budget, O, beta)
@@ -267,7 +295,8 @@ def evict_layer_from_scores(p_raw, p_ext_raw, imp, n_t, layer, w) -> LayerResult
     """select_layer with the hyper-parameters of a workload description `w`."""
     return select_layer(p_raw, p_ext_raw, imp, n_t, layer, T=w.seq_len, window=w.window,
                         window_ext=w.window_ext, budget=w.budget, pool_kernel=w.pool_kernel,
-                        delta=w.n_adjust_heads, lam=w.lam, beta=w.beta)
+                        delta=w.n_adjust_heads, lam=w.lam, beta=w.beta,
+                        criterion=getattr(w, "criterion", "std"))
 
 
 def score_layer(q_win: np.ndarray, k: np.ndarray, window: int):

@@ -26,6 +26,8 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   if (!(c->lambda >= 0.f) || !isfinite(c->lambda)) return KVEC_ERR_INVALID;
   if (!(c->beta >= 0.f && c->beta <= 1.f)) return KVEC_ERR_INVALID;
   if (c->dtype != KVEC_BF16 && c->dtype != KVEC_F32) return KVEC_ERR_INVALID;
+  if (c->head_criterion != KVEC_HEADS_STD && c->head_criterion != KVEC_HEADS_ENTROPY)
+    return KVEC_ERR_INVALID;
   if (c->head_dim < 1) return KVEC_ERR_INVALID;
   const int H = c->n_kv_heads, G = c->n_q_heads / c->n_kv_heads;
   if (H != 1 && H != 2 && H != 4 && H != 8) return KVEC_ERR_UNSUPPORTED;
@@ -54,6 +56,7 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   x.pool = c->pool_kernel;
   x.delta_eff = x.Wn > x.O ? c->n_adjust_heads : 0;
   x.lam = c->lambda;
+  x.criterion = c->head_criterion;
   x.sc = (float)(1.4426950408889634 / sqrt((double)x.D));
   x.inv_go = (float)(1.0 / ((double)G * x.O));
   x.inv_gwn = (float)(1.0 / ((double)G * x.Wn));

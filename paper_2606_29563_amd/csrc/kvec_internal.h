@@ -76,6 +76,7 @@ struct Problem {
   int esize;
   int n_gather;  // gather work-groups per (layer, sequence)
   int mcap;      // selection members per head held in LDS
+  int criterion; // H_top criterion: 0 lowest sigma, 1 highest entropy of pooled P
 };
 
 struct Geometry {
@@ -180,8 +181,10 @@ __device__ __forceinline__ int block_excl_scan(int v, int* tmp, int& total) {
 __host__ __device__ inline int pool_groups(const Problem& P) { return (P.n_pool + kPoolPer - 1) / kPoolPer; }
 
 // H_top (Sec. 4.1): bit h set for the delta_eff heads of sequence b with the
-// lowest variance of pooled P (ties: lower head), from the per-work-group
-// float64 sums of the pool stage.  Every caller computes it the same way, so
+// lowest variance of pooled P, or with the highest entropy of pooled P taken
+// as a distribution (the ablation's alternative, Sec. 5.4); ties: lower head.
+// From the per-work-group float64 sums of the pool stage: (sum, sum of
+// squares), or (sum S, sum of x ln x = Q), whence entropy = ln S - Q / S.  Every caller computes it the same way, so
 // the score passes of the extended window and the selection agree.  Each wave
 // computes it on its own (no LDS, no barrier): a power-of-two group of lanes
 // per head adds that head's partials (lane-strided, then a butterfly within
@@ -205,7 +208,8 @@ __device__ __forceinline__ uint32_t htop_mask(const Problem& P, const double2* s
     a2 += __shfl_xor(a2, o);
   }
   const double mean = a1 / P.Tc;
-  const double var = a2 / P.Tc - mean * mean;
+  // ranking key, lowest first: the variance, or minus the entropy
+  const double var = P.criterion ? (a1 > 0.0 ? a2 / a1 - log(a1) : 0.0) : a2 / P.Tc - mean * mean;
   int rank = 0;
   for (int o = 0; o < P.H; ++o) {
     const double vo = __shfl(var, o * lph);

@@ -179,7 +179,8 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
       if (want_p) {
         io.pooled[row + t] = m;
         s1 += (double)m;
-        s2 += (double)m * (double)m;
+        // sigma: sum of squares; entropy: sum of x ln x (0 ln 0 = 0)
+        s2 += P.criterion ? (m > 0.f ? (double)m * log((double)m) : 0.0) : (double)m * (double)m;
         atomicAdd(&hp[float_key(m) >> (32 - kHistBits)], 1u);
       }
       if (want_e) {

@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libkvec.so")
 
 KVEC_OK, KVEC_ERR_INVALID, KVEC_ERR_UNSUPPORTED, KVEC_ERR_WORKSPACE, KVEC_ERR_DEVICE = range(5)
 KVEC_BF16, KVEC_F32 = 0, 1
+KVEC_HEADS_STD, KVEC_HEADS_ENTROPY = 0, 1
 
 
 class KvecError(RuntimeError):
@@ -32,7 +33,7 @@ class kvec_config(ctypes.Structure):
         ("budget", ctypes.c_int32), ("pool_kernel", ctypes.c_int32),
         ("n_adjust_heads", ctypes.c_int32),
         ("lambda_", ctypes.c_float), ("beta", ctypes.c_float),
-        ("dtype", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("head_criterion", ctypes.c_int32),
     ]
 
 
@@ -53,12 +54,13 @@ class Config:
     lam: float = 1.0
     beta: float = 0.25
     dtype: int = KVEC_BF16
+    head_criterion: int = KVEC_HEADS_STD
 
     def c(self) -> kvec_config:
         return kvec_config(self.batch, self.n_layers, self.n_kv_heads, self.n_q_heads,
                            self.head_dim, self.seq_len, self.window, self.window_ext,
                            self.budget, self.pool_kernel, self.n_adjust_heads, self.lam,
-                           self.beta, self.dtype)
+                           self.beta, self.dtype, self.head_criterion)
 
     @classmethod
     def from_workload(cls, w, **over) -> "Config":
@@ -66,7 +68,9 @@ class Config:
                   n_q_heads=w.n_q_heads, head_dim=w.head_dim, seq_len=w.seq_len,
                   window=w.window, window_ext=w.window_ext, budget=w.budget,
                   pool_kernel=w.pool_kernel, n_adjust_heads=w.n_adjust_heads, lam=w.lam,
-                  beta=w.beta, dtype=KVEC_BF16 if w.dtype == "bf16" else KVEC_F32)
+                  beta=w.beta, dtype=KVEC_BF16 if w.dtype == "bf16" else KVEC_F32,
+                  head_criterion=KVEC_HEADS_ENTROPY if getattr(w, "criterion", "std") == "entropy"
+                  else KVEC_HEADS_STD)
         kw.update(over)
         return cls(**kw)
 

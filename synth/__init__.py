@@ -99,6 +99,7 @@ class Workload:
     n_adjust_heads: int = 3   # delta
     lam: float = 1.0          # lambda
     beta: float = 0.25
+    criterion: str = "std"    # head focus criterion of H_top: "std" or "entropy"
 
     @property
     def group(self) -> int:

@@ -71,6 +71,8 @@ def test_workspace_size_positive_and_monotone():
     (dict(lam=float("nan")), kvec.KVEC_ERR_INVALID),
     (dict(beta=1.5), kvec.KVEC_ERR_INVALID),
     (dict(dtype=7), kvec.KVEC_ERR_INVALID),
+    (dict(head_criterion=2), kvec.KVEC_ERR_INVALID),
+    (dict(head_criterion=-1), kvec.KVEC_ERR_INVALID),
     (dict(head_dim=96), kvec.KVEC_ERR_UNSUPPORTED),
     (dict(n_q_heads=72), kvec.KVEC_ERR_UNSUPPORTED),        # G = 9
     (dict(n_kv_heads=16, n_q_heads=32), kvec.KVEC_ERR_UNSUPPORTED),

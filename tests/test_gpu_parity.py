@@ -22,11 +22,11 @@ def _say(*a):
 
 
 def _small(name, T, O, Wn, H, G, D, dtype, batch=1, B=None, layers=2, pool=7, delta=3, lam=1.0,
-           beta=0.25, hh=0.02, rope=True, seed=7):
+           beta=0.25, hh=0.02, rope=True, seed=7, criterion="std"):
     B = B if B is not None else max(O + 8, T // 8)
     return synth.Workload(name, layers, H, H * G, D, T, batch, O, Wn, B, pool, dtype, seed,
                           rope=rope, hh_count=int(round(hh * T)), n_adjust_heads=min(delta, H),
-                          lam=lam, beta=beta)
+                          lam=lam, beta=beta, criterion=criterion)
 
 
 SCORE_CASES = [
@@ -88,6 +88,10 @@ SELECT_CASES = [
     _small("sel-wn-eq-o", 1500, 16, 16, 4, 2, 64, "bf16", B=100, layers=3),
     _small("sel-ragged", 999, 7, 14, 2, 1, 64, "bf16", B=41, layers=3, pool=3),
     _small("sel-long", 20000, 32, 64, 8, 4, 128, "bf16", B=700, layers=3),
+    # the entropy criterion of the head-selection ablation
+    _small("sel-entropy", 4096, 32, 64, 8, 4, 128, "bf16", B=128, layers=4, criterion="entropy"),
+    _small("sel-entropy-b2-d2", 3000, 64, 128, 4, 4, 128, "bf16", batch=2, B=300, layers=3,
+           pool=5, delta=2, criterion="entropy"),
 ]
 
 
@@ -247,6 +251,11 @@ def test_e2e_tiny_fp32(gpu_lib):
 
 def test_e2e_small_bf16(gpu_lib):
     _e2e(gpu_lib, _small("e2e-small", 2500, 32, 64, 8, 4, 128, "bf16", B=200, layers=6))
+
+
+def test_e2e_entropy_bf16(gpu_lib):
+    _e2e(gpu_lib, _small("e2e-entropy", 2500, 32, 64, 8, 4, 128, "bf16", B=200, layers=6,
+                         criterion="entropy"))
 
 
 def test_e2e_group7_bf16(gpu_lib):

@@ -267,8 +267,87 @@ def check_lowest_sigma(adjusted_heads):
     assert list(adjusted_heads(s, 9)) == [0, 1, 2, 3, 4]
 
 
+def check_entropy_closed_forms(head_entropy):
+    """Uniform scores: ln N.  One non-zero score: 0.  k scores of a and N-k of b:
+    with u = k*a + (N-k)*b, H = -(k*a/u) ln(a/u) - ((N-k)*b/u) ln(b/u).  Scaling a
+    head's scores does not change its entropy (they are normalised first)."""
+    N = 40
+    x = np.zeros((4, N), dtype=np.float32)
+    x[0] = 0.25
+    x[1, 7] = 3.0
+    a, b, k = 0.5, 0.125, 9
+    x[2, :k] = a
+    x[2, k:] = b
+    x[3] = x[2] * 8.0
+    got = head_entropy(x)
+    u = k * a + (N - k) * b
+    want2 = -(k * a / u) * math.log(a / u) - ((N - k) * b / u) * math.log(b / u)
+    assert abs(got[0] - math.log(N)) <= 1e-14
+    assert got[1] == 0.0
+    assert abs(got[2] - want2) <= 1e-14
+    assert abs(got[3] - want2) <= 1e-14
+
+
+def check_entropy_brute(head_entropy):
+    r = _rng(23)
+    x = r.random((3, 57)).astype(np.float32)
+    x[1, ::5] = 0.0
+    got = head_entropy(x)
+    for h in range(3):
+        tot = math.fsum(float(v) for v in x[h])
+        want = -math.fsum((float(v) / tot) * math.log(float(v) / tot) for v in x[h] if v > 0)
+        assert abs(got[h] - want) <= 1e-13
+
+
+def check_entropy_picks_least_focused(focus_heads):
+    """The entropy criterion takes the delta HIGHEST-entropy heads (the least
+    focused); sigma and entropy can disagree, so build heads where they do.
+    Head 0: uniform; head 1: one spike; head 2: two equal spikes on a floor;
+    head 3: a half-and-half two-level head scaled up (large sigma, high entropy)."""
+    N = 64
+    x = np.full((4, N), 1e-6, dtype=np.float32)
+    x[0] = 0.01
+    x[1, 3] = 1.0
+    x[2, 5] = x[2, 9] = 0.5
+    x[3, :32] = 10.0
+    x[3, 32:] = 5.0
+    ent = orc.head_entropy(x)
+    sig = orc.head_sigma(x)
+    assert list(np.argsort(-ent, kind="stable")[:2]) == [0, 3]
+    assert list(np.argsort(sig, kind="stable")[:2]) == [0, 2]      # sigma disagrees on head 3
+    assert list(focus_heads(x, 2, "entropy")) == [0, 3]
+    assert list(focus_heads(x, 2, "std")) == [0, 2]
+    y = np.stack([x[0], x[0], x[1]])                                  # tie -> lower head
+    assert list(focus_heads(y, 1, "entropy")) == [0]
+
+
 def test_sigma_population_std():
     check_sigma(orc.head_sigma)
+
+
+def test_entropy_closed_forms():
+    check_entropy_closed_forms(orc.head_entropy)
+
+
+def test_entropy_brute_force():
+    check_entropy_brute(orc.head_entropy)
+
+
+def test_entropy_picks_least_focused():
+    check_entropy_picks_least_focused(orc.focus_heads)
+
+
+def test_entropy_criterion_inert_when_every_head_adjusted():
+    """delta = H replaces every head whatever the criterion: same selection."""
+    r = _rng(24)
+    H, T, O = 4, 300, 8
+    p = r.random((H, T - O)).astype(np.float32) * 1e-3
+    pe = r.random((H, T - O)).astype(np.float32) * 1e-3
+    imp = r.random(T - O).astype(np.float32) * 1e-3
+    kw = dict(T=T, window=O, window_ext=16, budget=40, pool_kernel=3, lam=1.0, beta=0.25)
+    a = orc.select_layer(p, pe, imp, np.zeros(T, np.int64), 1, delta=H, criterion="std", **kw)
+    b = orc.select_layer(p, pe, imp, np.zeros(T, np.int64), 1, delta=H, criterion="entropy", **kw)
+    np.testing.assert_array_equal(a.idx, b.idx)
 
 
 def test_adjusted_heads_lowest_sigma():
@@ -553,6 +632,21 @@ def _mut_lse_no_scale(q_win, k):
     return orc.window_lse(q_win * math.sqrt(d), k)            # mistake: scale 1/sqrt(d) dropped
 
 
+def _mut_entropy_unnormalised(p):
+    x = np.asarray(p, dtype=np.float64)
+    out = np.zeros(x.shape[0])
+    for h in range(x.shape[0]):
+        q = x[h][x[h] > 0]                                    # mistake: not divided by the sum
+        out[h] = -(q * np.log(q)).sum()
+    return out
+
+
+def _mut_entropy_lowest(pooled, delta, criterion="std"):
+    if criterion == "entropy":
+        return orc.adjusted_heads(orc.head_entropy(pooled), delta)   # mistake: most focused
+    return orc.focus_heads(pooled, delta, criterion)
+
+
 def _mut_highest_sigma(sigma, delta):
     order = sorted(range(len(sigma)), key=lambda h: (-float(sigma[h]), h))   # mistake
     return np.array(sorted(order[:delta]), dtype=np.int64)
@@ -609,6 +703,9 @@ def _mut_preserve_raw(p_raw, p_ext_raw, imp, n_t, layer, **kw):
     (check_lse_brute, _mut_lse_no_causal),
     (check_lse_normalises_scores, _mut_lse_no_scale),
     (check_lowest_sigma, _mut_highest_sigma),
+    (check_entropy_closed_forms, _mut_entropy_unnormalised),
+    (check_entropy_brute, _mut_entropy_unnormalised),
+    (check_entropy_picks_least_focused, _mut_entropy_lowest),
     (check_bonus_hand, _mut_layer_denominator),
     (check_sigma, _mut_sample_std),
     (check_rank_brute, _mut_rank_index_desc),
