@@ -274,6 +274,32 @@ def main():
         print(f"[bench] {args.steps} steps in {wall:.2f} ms", file=sys.stderr, flush=True)
         roof = roofline(durs, n_launch, measured_traffic(w.name))
 
+    dec_obj = None
+    if args.path == "both":
+        # Decode attention over the compacted cache of the last step: one new
+        # token, every layer (the consumer of the cache the step writes).
+        g = torch.Generator().manual_seed(77)
+        qd = torch.randn((L, b, HQ, d), generator=g).to(dt).to(dev)
+        outd = torch.empty((L, b, HQ, d), dtype=torch.float32, device=dev)
+        wsd = torch.empty(kvec.kvec_decode_workspace_size(cfg, B), dtype=torch.uint8, device=dev)
+
+        def decode_all():
+            for l in range(L):
+                kvec.kvec_decode_attention(cfg, qd[l], ko[l], vo[l], outd[l], wsd, idx=idx[l])
+
+        durs, _ = time_steps(hip, stream, decode_all, max(args.steps, 20), args.warmup)
+        us = sum(durs) / len(durs) / L * 1e3
+        dbytes = b * (2 * H * B * d * es + HQ * d * es + HQ * d * 4 + H * B * 4)
+        dec_obj = {"entry": "kvec_decode_attention",
+                   "what": "one decode token's attention over the compacted cache, per layer "
+                           "(two launches: partial chunks, combine)",
+                   "us_per_layer": round(us, 2), "cache_rows": B,
+                   "roofline": {"bound": "hbm", "achieved": round(dbytes / (us * 1e-6) / 1e9, 1),
+                                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                "frac": round(dbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                                "algorithmic_bytes_per_call": dbytes}}
+        print(f"[bench] decode attention: {us:.2f} us per layer", file=sys.stderr, flush=True)
+
     lse_obj = None
     if args.path in ("both", "lse"):
         print("[bench] window-row log-sum-exp (prefill attention stand-in)", file=sys.stderr,
@@ -320,6 +346,8 @@ def main():
         out["config"]["entry"] = "kvec_evict_model_lse"
     elif lse_obj is not None:
         out["prefill_lse_step"] = lse_obj
+    if dec_obj is not None:
+        out["decode_attention"] = dec_obj
     print(json.dumps(out))
 
 

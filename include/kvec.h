@@ -24,6 +24,10 @@
  *   kvec_evict_model  the whole prefill eviction step for all layers.
  *   kvec_coverage     the coverage C = number of unique tokens kept across
  *                     heads and layers (Sec. 3.2).
+ *   kvec_decode_attention
+ *                     the consumer of the compacted cache: one decode token's
+ *                     attention over the kept K/V (Sec. 4.1 keeps them for the
+ *                     decoding phase).
  *   kvec_score_lse, kvec_evict_model_lse
  *                     the same scores and step when the caller already holds
  *                     the softmax normaliser of every window row: K-VEC runs
@@ -229,6 +233,34 @@ int32_t kvec_profile_points_lse(const kvec_config* cfg);
  *   count_per_seq  device out, int64 [batch]. */
 kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits,
                           int32_t upto_layer, int64_t* count_per_seq, hipStream_t stream);
+
+/* Workspace bytes of kvec_decode_attention for `cfg` and n_ctx cache rows
+ * (host-only).  n_ctx in 1..2^20. */
+kvec_status kvec_decode_workspace_size(const kvec_config* cfg, int32_t n_ctx, size_t* bytes);
+
+/* Decode-step attention over the compacted cache (the kept K/V of Sec. 4.1
+ * serve the decoding phase).  For every sequence b and query head j:
+ *   out[b][j] = sum_i softmax_i(q_j . k_{h,i} / sqrt(d)) v_{h,i},  h = j / G,
+ * over the cache rows i < n_ctx of KV head h, leaving out rows i < B whose
+ * idx is negative (the padding kvec_compact writes when T <= B).
+ *   q             device, cfg->dtype [batch][n_q_heads][d] (the new token's
+ *                 post-RoPE queries), strides q_strides = {batch, head}.
+ *   k_cache, v_cache  device, cfg->dtype [batch][H][n_ctx][d] with strides
+ *                 cache_strides = {batch, head}, rows contiguous: the
+ *                 compacted cache (rows 0..B-1 as kvec_compact writes them;
+ *                 rows B.. may hold tokens appended after the prefill).
+ *   n_ctx         rows per (sequence, head), 1..2^20 (>= B when idx is given).
+ *   idx           nullable device int32 [batch][H][B] (kvec_compact's idx).
+ *   out           device out, fp32 [batch][n_q_heads][d], contiguous; a
+ *                 head with no unmasked row gets zeros.
+ *   ws            device workspace of kvec_decode_workspace_size() bytes.
+ * Errors as elsewhere (alignment 16 bytes for q and the caches, 4 for out). */
+kvec_status kvec_decode_attention(const kvec_config* cfg,
+                                  const void* q, const int64_t q_strides[2],
+                                  const void* k_cache, const void* v_cache,
+                                  const int64_t cache_strides[2], int32_t n_ctx,
+                                  const int32_t* idx, float* out,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Static description of a status code. */
 const char* kvec_status_string(kvec_status status);

@@ -21,6 +21,7 @@ of LLM" (K-VEC).  Each function names the passage it follows:
 * focus = I * (1 - coverage); P' = P + lambda*focus  Sec. 4.2; Algorithm 1
 * top beta*B tokens of P per head get P' = 1.0     Sec. 4.2; Algorithm 1
 * coverage C = number of unique kept tokens       Sec. 3.2
+* decode attention over the kept K/V              Sec. 4.1 (the cache serves decoding)
 
 Readings where the paper is silent (each is listed in the design notes):
 heads are KV heads and A of a KV head is the mean over its query heads (GQA);
@@ -45,7 +46,7 @@ import numpy as np
 
 __all__ = [
     "window_attention", "window_lse", "window_scores", "to_f32", "maxpool1d", "head_sigma",
-    "head_entropy", "focus_heads",
+    "head_entropy", "focus_heads", "decode_attention",
     "adjusted_heads", "rank_first", "preserve_count", "adjusted_priority",
     "LayerResult", "select_layer", "evict_layer_from_scores", "score_layer",
     "gather_rows", "coverage_count", "counts_from_bits", "layer_bits",
@@ -339,4 +340,29 @@ def gather_rows(x: np.ndarray, idx: np.ndarray) -> np.ndarray:
     for h in range(H):
         ok = idx[h] >= 0
         out[h, ok] = x[h, idx[h, ok]]
+    return out
+
+
+# ---------------------------------------------------------------------------
+# After the step: one decode token's attention over the compacted cache
+# ---------------------------------------------------------------------------
+
+def decode_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, valid=None) -> np.ndarray:
+    """Softmax attention of one new token over the kept cache rows (float64).
+
+    q: [H_q][d]; k, v: [H_kv][n][d]; valid: [H_kv][n] bool or None (all rows).
+    out[j] = sum_i softmax_i(q_j . k_{j//G,i} / sqrt(d)) v_{j//G,i} over the
+    valid rows i of KV head j // G; a head with no valid row gives zeros."""
+    hq, d = q.shape
+    hkv = k.shape[0]
+    g = hq // hkv
+    out = np.zeros((hq, d))
+    for j in range(hq):
+        h = j // g
+        rows = np.arange(k.shape[1]) if valid is None else np.nonzero(valid[h])[0]
+        if len(rows) == 0:
+            continue
+        s = (k[h, rows] @ q[j]) / math.sqrt(d)
+        e = np.exp(s - s.max())
+        out[j] = (e / e.sum()) @ v[h, rows]
     return out

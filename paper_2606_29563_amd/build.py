@@ -15,7 +15,8 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 
 # (source, object name, extra flags): the step kernel is instantiated once per
 # (dtype, head_dim) pair, in parallel translation units
-SOURCES = [("kvec_api.hip", "kvec_api", []), ("kvec_pipeline.hip", "kvec_pipeline", [])] + [
+SOURCES = [("kvec_api.hip", "kvec_api", []), ("kvec_pipeline.hip", "kvec_pipeline", []),
+           ("kvec_decode.hip", "kvec_decode", [])] + [
     ("kvec_step_inst.hip", f"kvec_step_{tt.lower()}_d{d}", [f"-DKVEC_INST_TT={tt}", f"-DKVEC_INST_D={d}"])
     for tt in ("BF16", "F32") for d in (64, 128)]
 

@@ -419,6 +419,35 @@ int32_t kvec_profile_points(const kvec_config* cfg) {
   return g.keep_all ? 0 : g.p.L + kPipeDepth + 1;
 }
 
+kvec_status kvec_decode_workspace_size(const kvec_config* cfg, int32_t n_ctx, size_t* bytes) {
+  Geometry g;
+  const kvec_status st = make_geometry(cfg, &g);
+  if (st != KVEC_OK) return st;
+  if (!bytes || n_ctx < 1 || n_ctx > (1 << 20)) return KVEC_ERR_INVALID;
+  *bytes = decode_plan(g.p, n_ctx).ws_bytes;
+  return KVEC_OK;
+}
+
+kvec_status kvec_decode_attention(const kvec_config* cfg, const void* q, const int64_t q_strides[2],
+                                  const void* k_cache, const void* v_cache,
+                                  const int64_t cache_strides[2], int32_t n_ctx,
+                                  const int32_t* idx, float* out, void* ws, size_t ws_bytes,
+                                  hipStream_t stream) {
+  Geometry g;
+  const kvec_status st = make_geometry(cfg, &g);
+  if (st != KVEC_OK) return st;
+  if (n_ctx < 1 || n_ctx > (1 << 20) || (idx && n_ctx < g.p.B)) return KVEC_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !out ||
+      ((uintptr_t)out & 3u) != 0 || !strides_ok(q_strides, 2, g.p.esize) ||
+      !strides_ok(cache_strides, 2, g.p.esize))
+    return KVEC_ERR_INVALID;
+  const DecodePlan pl = decode_plan(g.p, n_ctx);
+  if (ws_bytes < pl.ws_bytes) return KVEC_ERR_WORKSPACE;
+  if (!aligned16(ws)) return KVEC_ERR_INVALID;
+  return dev(run_decode(g, q, q_strides, k_cache, v_cache, cache_strides, n_ctx, idx, out, ws,
+                        stream));
+}
+
 int32_t kvec_profile_points_lse(const kvec_config* cfg) {
   Geometry g;
   if (make_geometry(cfg, &g) != KVEC_OK) return -1;

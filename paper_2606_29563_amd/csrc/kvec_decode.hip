@@ -1,0 +1,273 @@
+// Decode-step attention over the compacted cache.
+//
+// The eviction step stores the kept K/V of every KV head (Sec. 4.1); the
+// decoding phase then attends from each new token's query heads to those
+// rows.  For one decode token, query head j of sequence b computes
+//   out[b][j] = sum_i softmax_i(q_j . k_i / sqrt(d)) v_i
+// over the rows i of its KV head j / G, leaving out the padding rows that
+// kvec_compact writes when T <= B (idx -1).
+//
+// The work is bound by reading the cache once.  Two launches:
+//   partial  one work-group per (row chunk, KV head, sequence): the G query
+//            heads of the KV head share every K/V row read.  A row is read by
+//            a group of lanes, 16 bytes each (fully coalesced), the group's
+//            partial dot products are summed with lane shuffles, and each
+//            lane keeps an online-softmax state (max, sum, weighted V
+//            elements) per query head.  States merge across the row groups
+//            of a wave by shuffles, across waves through LDS, and the
+//            chunk's (max, sum, V[d]) go to the workspace.
+//   combine  one work-group per (query head, sequence) merges the chunks.
+#include <math.h>
+
+#include "kvec_internal.h"
+
+namespace kvec {
+namespace {
+
+constexpr int kDecThreads = 256;        // 4 waves per partial work-group
+constexpr int kDecWaves = kDecThreads / 64;
+constexpr int kDecUnroll = 4;           // rows in flight per lane group
+
+template <class T>
+struct DecElem;
+template <>
+struct DecElem<__bf16> {
+  static constexpr int N = 8;  // elements per 16-byte piece
+  __device__ static void unpack(const uint4& u, float (&f)[N]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = __uint_as_float(w[i] << 16);
+      f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+};
+template <>
+struct DecElem<float> {
+  static constexpr int N = 4;
+  __device__ static void unpack(const uint4& u, float (&f)[N]) {
+    f[0] = __uint_as_float(u.x);
+    f[1] = __uint_as_float(u.y);
+    f[2] = __uint_as_float(u.z);
+    f[3] = __uint_as_float(u.w);
+  }
+};
+
+struct DecArgs {
+  const char* q;
+  int64_t qs_b, qs_h;   // elements
+  const char* k;
+  const char* v;
+  int64_t cs_b, cs_h;   // elements; rows contiguous (d elements apart)
+  const int32_t* idx;   // nullable [b][H][B]
+  float* part;          // [b][HQ][S][D + 2]
+  float* out;           // [b][HQ][D]
+  int H, HQ, B, n_ctx, chunk, S;
+  float sc;             // log2(e) / sqrt(d)
+};
+
+// Merge (m2, l2, a2) into (m, l, a); m = -inf means an empty state.
+__device__ __forceinline__ void dec_merge(float& m, float& l, float* a, float m2, float l2,
+                                          const float* a2, int n) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -INFINITY) return;
+  const float f1 = __builtin_amdgcn_exp2f(m - mm), f2 = __builtin_amdgcn_exp2f(m2 - mm);
+  l = l * f1 + l2 * f2;
+  for (int e = 0; e < n; ++e) a[e] = a[e] * f1 + a2[e] * f2;
+  m = mm;
+}
+
+template <class T, int D, int G>
+__global__ __launch_bounds__(kDecThreads) void decode_partial(DecArgs a) {
+  using E = DecElem<T>;
+  constexpr int EPL = E::N;            // elements of d per lane
+  constexpr int LPR = D / EPL;         // lanes per row
+  constexpr int RPW = 64 / LPR;        // rows per wave and round
+  __shared__ float sm[kDecWaves][G][2];
+  __shared__ float sa[kDecWaves][G][D];
+  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int grp = lane / LPR, pc = lane % LPR;  // row group, piece of the row
+  const int r0 = s * a.chunk, r1 = min(a.n_ctx, r0 + a.chunk);
+
+  float qv[G][EPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const uint4 u = reinterpret_cast<const uint4*>(
+        a.q + ((int64_t)b * a.qs_b + (int64_t)(h * G + g) * a.qs_h) * sizeof(T))[pc];
+    E::unpack(u, qv[g]);
+  }
+  float m[G], l[G], acc[G][EPL];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    m[g] = -INFINITY;
+    l[g] = 0.f;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
+  }
+  const char* kb = a.k + ((int64_t)b * a.cs_b + (int64_t)h * a.cs_h) * sizeof(T);
+  const char* vb = a.v + ((int64_t)b * a.cs_b + (int64_t)h * a.cs_h) * sizeof(T);
+  const int32_t* ib = a.idx ? a.idx + ((int64_t)b * a.H + h) * a.B : nullptr;
+  constexpr int kStep = kDecWaves * RPW;  // rows per round of the work-group
+  for (int base = r0; base < r1; base += kStep * kDecUnroll) {
+    uint4 ku[kDecUnroll], vu[kDecUnroll];
+    bool live[kDecUnroll];
+    // issue every load of the unrolled rounds first; the rows do not wait for
+    // their idx entries (every row below n_ctx is in bounds), the mask is
+    // applied once all of them have arrived
+#pragma unroll
+    for (int uu = 0; uu < kDecUnroll; ++uu) {
+      const int r = base + uu * kStep + w * RPW + grp;
+      live[uu] = r < r1;
+      ku[uu] = make_uint4(0, 0, 0, 0);
+      vu[uu] = make_uint4(0, 0, 0, 0);
+      if (live[uu]) {
+        ku[uu] = reinterpret_cast<const uint4*>(kb + (int64_t)r * D * sizeof(T))[pc];
+        vu[uu] = reinterpret_cast<const uint4*>(vb + (int64_t)r * D * sizeof(T))[pc];
+      }
+    }
+    if (ib) {
+#pragma unroll
+      for (int uu = 0; uu < kDecUnroll; ++uu) {
+        const int r = base + uu * kStep + w * RPW + grp;
+        if (live[uu] && r < a.B && ib[r] < 0) live[uu] = false;
+      }
+    }
+#pragma unroll
+    for (int uu = 0; uu < kDecUnroll; ++uu) {
+      float kf[EPL], vf[EPL];
+      E::unpack(ku[uu], kf);
+      E::unpack(vu[uu], vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float d = 0.f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) d = fmaf(qv[g][e], kf[e], d);
+#pragma unroll
+        for (int o = 1; o < LPR; o <<= 1) d += __shfl_xor(d, o);
+        if (!live[uu]) continue;  // uniform within the row group
+        const float x = d * a.sc;
+        const float mm = fmaxf(m[g], x);
+        const float f = __builtin_amdgcn_exp2f(m[g] - mm);
+        const float p = __builtin_amdgcn_exp2f(x - mm);
+        l[g] = l[g] * f + p;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e] * f);
+        m[g] = mm;
+      }
+    }
+  }
+  // merge the RPW row groups of the wave (lanes with the same piece)
+#pragma unroll
+  for (int o = LPR; o < 64; o <<= 1) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float a2[EPL];
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) a2[e] = __shfl_xor(acc[g][e], o);
+      const float m2 = __shfl_xor(m[g], o), l2 = __shfl_xor(l[g], o);
+      dec_merge(m[g], l[g], acc[g], m2, l2, a2, EPL);
+    }
+  }
+  if (grp == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      if (pc == 0) {
+        sm[w][g][0] = m[g];
+        sm[w][g][1] = l[g];
+      }
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) sa[w][g][pc * EPL + e] = acc[g][e];
+    }
+  }
+  __syncthreads();
+  // merge the waves: thread (g, e) for every element of every query head
+  for (int t = threadIdx.x; t < G * D; t += kDecThreads) {
+    const int g = t / D, e = t % D;
+    float mm = -INFINITY, ll = 0.f, av = 0.f;
+    for (int ww = 0; ww < kDecWaves; ++ww) dec_merge(mm, ll, &av, sm[ww][g][0], sm[ww][g][1], &sa[ww][g][e], 1);
+    float* pp = a.part + (((int64_t)b * a.HQ + h * G + g) * a.S + s) * (D + 2);
+    pp[2 + e] = av;
+    if (e == 0) {
+      pp[0] = mm;
+      pp[1] = ll;
+    }
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void decode_combine(DecArgs a) {
+  const int j = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
+  const float* pp = a.part + ((int64_t)b * a.HQ + j) * a.S * (D + 2);
+  float m = -INFINITY, l = 0.f, av = 0.f;
+  for (int s = 0; s < a.S; ++s) dec_merge(m, l, &av, pp[s * (D + 2)], pp[s * (D + 2) + 1], &pp[s * (D + 2) + 2 + e], 1);
+  a.out[((int64_t)b * a.HQ + j) * D + e] = l > 0.f ? av / l : 0.f;
+}
+
+typedef void (*DecFn)(DecArgs);
+
+template <class T, int D>
+DecFn dec_pick(int G) {
+  switch (G) {
+    case 1: return decode_partial<T, D, 1>;
+    case 2: return decode_partial<T, D, 2>;
+    case 3: return decode_partial<T, D, 3>;
+    case 4: return decode_partial<T, D, 4>;
+    case 5: return decode_partial<T, D, 5>;
+    case 6: return decode_partial<T, D, 6>;
+    case 7: return decode_partial<T, D, 7>;
+    default: return decode_partial<T, D, 8>;
+  }
+}
+
+}  // namespace
+
+// Row chunk per work-group: enough work-groups to cover the chip (about
+// 512 over batch x heads), at least 64 rows each.
+DecodePlan decode_plan(const Problem& P, int n_ctx) {
+  DecodePlan d;
+  const int per = 512 / (P.batch * P.H) > 1 ? 512 / (P.batch * P.H) : 1;
+  int chunk = (n_ctx + per - 1) / per;
+  chunk = chunk < 64 ? 64 : (chunk + 63) / 64 * 64;
+  d.chunk = chunk;
+  d.S = (n_ctx + chunk - 1) / chunk;
+  d.ws_bytes = (size_t)P.batch * P.HQ * d.S * (P.D + 2) * 4;
+  return d;
+}
+
+hipError_t run_decode(const Geometry& g, const void* q, const int64_t qs[2], const void* k,
+                      const void* v, const int64_t cs[2], int n_ctx, const int32_t* idx, float* out,
+                      void* ws, hipStream_t s) {
+  const Problem& P = g.p;
+  const DecodePlan pl = decode_plan(P, n_ctx);
+  DecArgs a;
+  a.q = static_cast<const char*>(q);
+  a.qs_b = qs[0];
+  a.qs_h = qs[1];
+  a.k = static_cast<const char*>(k);
+  a.v = static_cast<const char*>(v);
+  a.cs_b = cs[0];
+  a.cs_h = cs[1];
+  a.idx = idx;
+  a.part = static_cast<float*>(ws);
+  a.out = out;
+  a.H = P.H;
+  a.HQ = P.HQ;
+  a.B = P.B;
+  a.n_ctx = n_ctx;
+  a.chunk = pl.chunk;
+  a.S = pl.S;
+  a.sc = P.sc;
+  DecFn fn = P.esize == 2 ? (P.D == 64 ? dec_pick<__bf16, 64>(P.G) : dec_pick<__bf16, 128>(P.G))
+                          : (P.D == 64 ? dec_pick<float, 64>(P.G) : dec_pick<float, 128>(P.G));
+  hipLaunchKernelGGL(fn, dim3(pl.S, P.H, P.batch), dim3(kDecThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (P.D == 64)
+    hipLaunchKernelGGL(decode_combine<64>, dim3(P.HQ, P.batch), dim3(64), 0, s, a);
+  else
+    hipLaunchKernelGGL(decode_combine<128>, dim3(P.HQ, P.batch), dim3(128), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace kvec

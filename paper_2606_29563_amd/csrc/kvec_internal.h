@@ -127,6 +127,17 @@ hipError_t run_keep_all(const Geometry& g, int layer, uint64_t* bits, int32_t* i
 hipError_t run_coverage(const Geometry& g, const uint64_t* bits, int upto, int64_t* count,
                         hipStream_t s);
 
+// Decode attention over the compacted cache (kvec_decode.hip).
+struct DecodePlan {
+  int chunk;        // cache rows per partial work-group
+  int S;            // chunks per (sequence, KV head)
+  size_t ws_bytes;  // partial states [b][HQ][S][d + 2] floats
+};
+DecodePlan decode_plan(const Problem& P, int n_ctx);
+hipError_t run_decode(const Geometry& g, const void* q, const int64_t qs[2], const void* k,
+                      const void* v, const int64_t cs[2], int n_ctx, const int32_t* idx, float* out,
+                      void* ws, hipStream_t s);
+
 // ---------------------------------------------------------------------------
 // Device helpers
 // ---------------------------------------------------------------------------

@@ -88,7 +88,7 @@ _lib = None
 EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_score_lse", "kvec_select_cover",
            "kvec_compact", "kvec_evict_layer", "kvec_evict_model", "kvec_evict_model_lse",
            "kvec_profile_points", "kvec_profile_points_lse", "kvec_coverage",
-           "kvec_status_string"]
+           "kvec_decode_workspace_size", "kvec_decode_attention", "kvec_status_string"]
 
 
 def load() -> ctypes.CDLL:
@@ -114,6 +114,8 @@ def load() -> ctypes.CDLL:
     lib.kvec_evict_model_lse.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp,
                                          vp, sz, vp, ctypes.POINTER(vp)]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
+    lib.kvec_decode_workspace_size.argtypes = [P, i32, ctypes.POINTER(sz)]
+    lib.kvec_decode_attention.argtypes = [P, vp, I64x, vp, vp, I64x, i32, vp, vp, vp, sz, vp]
     lib.kvec_profile_points.argtypes = [P]
     lib.kvec_profile_points_lse.argtypes = [P]
     lib.kvec_status_string.argtypes = [ctypes.c_int]
@@ -256,3 +258,25 @@ def kvec_coverage(cfg: Config, cover_bits, upto_layer: int, count, stream=None) 
     c = cfg.c()
     _check(load().kvec_coverage(ctypes.byref(c), _ptr(cover_bits), upto_layer, _ptr(count),
                                 _stream(stream)), "kvec_coverage")
+
+
+def kvec_decode_workspace_size(cfg: Config, n_ctx: int) -> int:
+    out = ctypes.c_size_t(0)
+    c = cfg.c()
+    _check(load().kvec_decode_workspace_size(ctypes.byref(c), n_ctx, ctypes.byref(out)),
+           "kvec_decode_workspace_size")
+    return out.value
+
+
+def kvec_decode_attention(cfg: Config, q, k_cache, v_cache, out, ws, idx=None, n_ctx=None,
+                          stream=None) -> None:
+    """q [b][HQ][d]; k_cache/v_cache [b][H][n_ctx][d] (rows contiguous); out fp32 [b][HQ][d]."""
+    c = cfg.c()
+    n = k_cache.shape[2] if n_ctx is None else n_ctx
+    assert k_cache.stride()[:2] == v_cache.stride()[:2], "K and V caches share their strides"
+    assert k_cache.stride(2) == k_cache.shape[3] and v_cache.stride(2) == v_cache.shape[3], \
+        "cache rows must be contiguous"
+    _check(load().kvec_decode_attention(ctypes.byref(c), _ptr(q), _strides(q, 2), _ptr(k_cache),
+                                        _ptr(v_cache), _strides(k_cache, 2), n, _ptr(idx),
+                                        _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
+                                        _stream(stream)), "kvec_decode_attention")

@@ -133,6 +133,26 @@ def test_entry_points_reject_before_launch():
                                     None) == kvec.KVEC_ERR_WORKSPACE
 
 
+def test_decode_validation():
+    lib = kvec.load()
+    c = _cfg().c()
+    fake = ctypes.c_void_p(1 << 20)
+    qs = (ctypes.c_int64 * 2)(32 * 128, 128)
+    cs = (ctypes.c_int64 * 2)(8 * 1024 * 128, 1024 * 128)
+    ok = dict(n=1024, ws=1 << 40)
+    assert kvec.kvec_decode_workspace_size(_cfg(), 1024) > 0
+    def call(q=fake, kc=fake, n=1024, idx=None, out=fake, ws_bytes=1 << 40, cstr=cs):
+        return lib.kvec_decode_attention(ctypes.byref(c), q, qs, kc, fake, cstr, n, idx, out, fake,
+                                         ws_bytes, None)
+    assert call(n=0) == kvec.KVEC_ERR_INVALID
+    assert call(n=(1 << 20) + 1) == kvec.KVEC_ERR_INVALID
+    assert call(n=1000, idx=fake) == kvec.KVEC_ERR_INVALID        # idx needs n_ctx >= B
+    assert call(q=ctypes.c_void_p((1 << 20) + 4)) == kvec.KVEC_ERR_INVALID
+    assert call(out=None) == kvec.KVEC_ERR_INVALID
+    assert call(cstr=(ctypes.c_int64 * 2)(8 * 1024 * 128, 1024 * 128 + 1)) == kvec.KVEC_ERR_INVALID
+    assert call(ws_bytes=16) == kvec.KVEC_ERR_WORKSPACE
+
+
 def test_profile_points():
     assert kvec.kvec_profile_points(_cfg()) == 32 + 11
     assert kvec.kvec_profile_points_lse(_cfg()) == 32 + 7

@@ -178,6 +178,63 @@ def test_lse_normalises_scores():
     check_lse_normalises_scores(orc.window_lse)
 
 
+def check_decode_constant_keys(decode_attention):
+    """All keys of a head equal: uniform weights, so out = the mean of the valid
+    V rows; distinct keys per head pin the query-to-KV-head map through V."""
+    r = _rng(25)
+    hkv, g, n, d = 2, 3, 11, 8
+    k = np.repeat(r.standard_normal((hkv, 1, d)), n, axis=1)
+    v = r.standard_normal((hkv, n, d))
+    q = r.standard_normal((hkv * g, d))
+    valid = np.ones((hkv, n), bool)
+    valid[1, [0, 4, 5]] = False
+    out = decode_attention(q, k, v, valid)
+    for j in range(hkv * g):
+        want = v[j // g][valid[j // g]].mean(axis=0)
+        np.testing.assert_allclose(out[j], want, rtol=1e-13, atol=1e-15)
+
+
+def check_decode_brute(decode_attention):
+    r = _rng(26)
+    hkv, g, n, d = 2, 2, 7, 4
+    q = r.standard_normal((hkv * g, d)) * 2
+    k = r.standard_normal((hkv, n, d)) * 2
+    v = r.standard_normal((hkv, n, d))
+    valid = r.random((hkv, n)) > 0.3
+    out = decode_attention(q, k, v, valid)
+    for j in range(hkv * g):
+        h = j // g
+        logits = [math.fsum(q[j, i] * k[h, t, i] for i in range(d)) / math.sqrt(d)
+                  for t in range(n) if valid[h, t]]
+        vs = [v[h, t] for t in range(n) if valid[h, t]]
+        mx = max(logits)
+        ex = [math.exp(x - mx) for x in logits]
+        z = math.fsum(ex)
+        for c in range(d):
+            want = math.fsum(ex[i] / z * vs[i][c] for i in range(len(vs)))
+            assert abs(out[j, c] - want) <= 1e-12
+
+
+def test_decode_constant_keys():
+    check_decode_constant_keys(orc.decode_attention)
+
+
+def test_decode_brute_force():
+    check_decode_brute(orc.decode_attention)
+
+
+def test_decode_single_row_and_empty():
+    r = _rng(27)
+    q = r.standard_normal((2, 4))
+    k = r.standard_normal((1, 5, 4))
+    v = r.standard_normal((1, 5, 4))
+    valid = np.zeros((1, 5), bool)
+    np.testing.assert_array_equal(orc.decode_attention(q, k, v, valid), 0.0)
+    valid[0, 3] = True
+    np.testing.assert_allclose(orc.decode_attention(q, k, v, valid), np.stack([v[0, 3]] * 2),
+                               rtol=1e-15)
+
+
 def test_zero_query_closed_form():
     check_zero_query_closed_form(orc.window_scores)
 
@@ -647,6 +704,23 @@ def _mut_entropy_lowest(pooled, delta, criterion="std"):
     return orc.focus_heads(pooled, delta, criterion)
 
 
+def _mut_decode_head_map(q, k, v, valid=None):
+    hq, hkv = q.shape[0], k.shape[0]
+    out = np.zeros(q.shape)
+    for j in range(hq):                                       # mistake: j % H_kv, not j // G
+        out[j] = orc.decode_attention(q[j:j + 1], k[j % hkv:j % hkv + 1], v[j % hkv:j % hkv + 1],
+                                      None if valid is None else valid[j % hkv:j % hkv + 1])[0]
+    return out
+
+
+def _mut_decode_no_scale(q, k, v, valid=None):
+    return orc.decode_attention(q * math.sqrt(q.shape[1]), k, v, valid)   # mistake: no 1/sqrt(d)
+
+
+def _mut_decode_no_mask(q, k, v, valid=None):
+    return orc.decode_attention(q, k, v, None)                           # mistake: mask ignored
+
+
 def _mut_highest_sigma(sigma, delta):
     order = sorted(range(len(sigma)), key=lambda h: (-float(sigma[h]), h))   # mistake
     return np.array(sorted(order[:delta]), dtype=np.int64)
@@ -703,6 +777,10 @@ def _mut_preserve_raw(p_raw, p_ext_raw, imp, n_t, layer, **kw):
     (check_lse_brute, _mut_lse_no_causal),
     (check_lse_normalises_scores, _mut_lse_no_scale),
     (check_lowest_sigma, _mut_highest_sigma),
+    (check_decode_constant_keys, _mut_decode_head_map),
+    (check_decode_constant_keys, _mut_decode_no_mask),
+    (check_decode_brute, _mut_decode_no_scale),
+    (check_decode_brute, _mut_decode_head_map),
     (check_entropy_closed_forms, _mut_entropy_unnormalised),
     (check_entropy_brute, _mut_entropy_unnormalised),
     (check_entropy_picks_least_focused, _mut_entropy_lowest),
