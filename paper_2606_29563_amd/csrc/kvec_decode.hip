@@ -20,6 +20,7 @@
 #include <math.h>
 
 #include "kvec_internal.h"
+#include "kvec_score_dev.h"  // DPP lane moves
 
 namespace kvec {
 namespace {
@@ -67,14 +68,30 @@ struct DecArgs {
 };
 
 // Merge (m2, l2, a2) into (m, l, a); m = -inf means an empty state.
+// Branch-free, so the lane moves feeding a batch of merges stay in flight
+// together.
 __device__ __forceinline__ void dec_merge(float& m, float& l, float* a, float m2, float l2,
                                           const float* a2, int n) {
   const float mm = fmaxf(m, m2);
-  if (mm == -INFINITY) return;
-  const float f1 = __builtin_amdgcn_exp2f(m - mm), f2 = __builtin_amdgcn_exp2f(m2 - mm);
+  const float f1 = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mm);
+  const float f2 = m2 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
   l = l * f1 + l2 * f2;
   for (int e = 0; e < n; ++e) a[e] = a[e] * f1 + a2[e] * f2;
   m = mm;
+}
+
+// Sum over each aligned group of LPR lanes, every lane of the group getting
+// the total: quad swaps, the half-row mirror and the row rotation by 8 (DPP,
+// no LDS round trip), lane shuffles only across 16-lane rows.
+template <int LPR>
+__device__ __forceinline__ float group_sum(float v) {
+  if constexpr (LPR >= 2) v += dpp_f<kDppSwap1>(v);
+  if constexpr (LPR >= 4) v += dpp_f<kDppSwap2>(v);
+  if constexpr (LPR >= 8) v += dpp_f<kDppHalfMirror>(v);
+  if constexpr (LPR >= 16) v += dpp_f<kDppRor8>(v);
+  if constexpr (LPR >= 32) v += __shfl_xor(v, 16);
+  if constexpr (LPR >= 64) v += __shfl_xor(v, 32);
+  return v;
 }
 
 template <class T, int D, int G>
@@ -108,48 +125,55 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial(DecArgs a) {
   const char* kb = a.k + ((int64_t)b * a.cs_b + (int64_t)h * a.cs_h) * sizeof(T);
   const char* vb = a.v + ((int64_t)b * a.cs_b + (int64_t)h * a.cs_h) * sizeof(T);
   const int32_t* ib = a.idx ? a.idx + ((int64_t)b * a.H + h) * a.B : nullptr;
+  // without idx every lane reads word 0 of its K rows instead (unused), so
+  // the loads below need no branch
+  const int32_t* ibp = ib ? ib : reinterpret_cast<const int32_t*>(kb);
+  const int imax = ib ? a.B - 1 : 0;
   constexpr int kStep = kDecWaves * RPW;  // rows per round of the work-group
   for (int base = r0; base < r1; base += kStep * kDecUnroll) {
     uint4 ku[kDecUnroll], vu[kDecUnroll];
+    int iv[kDecUnroll];
     bool live[kDecUnroll];
-    // issue every load of the unrolled rounds first; the rows do not wait for
-    // their idx entries (every row below n_ctx is in bounds), the mask is
-    // applied once all of them have arrived
+    // issue every load of the unrolled rounds first, with no wait in between:
+    // the idx entries at clamped (in-bounds) positions, and the rows below
+    // n_ctx (all in bounds) whether or not idx masks them
 #pragma unroll
     for (int uu = 0; uu < kDecUnroll; ++uu) {
       const int r = base + uu * kStep + w * RPW + grp;
+      // rows past the chunk load the chunk's last row (never used)
+      const int rl = min(r, r1 - 1);
+      iv[uu] = ibp[min(r, imax)];
       live[uu] = r < r1;
-      ku[uu] = make_uint4(0, 0, 0, 0);
-      vu[uu] = make_uint4(0, 0, 0, 0);
-      if (live[uu]) {
-        ku[uu] = reinterpret_cast<const uint4*>(kb + (int64_t)r * D * sizeof(T))[pc];
-        vu[uu] = reinterpret_cast<const uint4*>(vb + (int64_t)r * D * sizeof(T))[pc];
-      }
-    }
-    if (ib) {
-#pragma unroll
-      for (int uu = 0; uu < kDecUnroll; ++uu) {
-        const int r = base + uu * kStep + w * RPW + grp;
-        if (live[uu] && r < a.B && ib[r] < 0) live[uu] = false;
-      }
+      ku[uu] = reinterpret_cast<const uint4*>(kb + (int64_t)rl * D * sizeof(T))[pc];
+      vu[uu] = reinterpret_cast<const uint4*>(vb + (int64_t)rl * D * sizeof(T))[pc];
     }
 #pragma unroll
     for (int uu = 0; uu < kDecUnroll; ++uu) {
+      const int r = base + uu * kStep + w * RPW + grp;
+      if (ib && r < a.B && iv[uu] < 0) live[uu] = false;
       float kf[EPL], vf[EPL];
       E::unpack(ku[uu], kf);
       E::unpack(vu[uu], vf);
+      float x[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float d = 0.f;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) d = fmaf(qv[g][e], kf[e], d);
+        x[g] = d;
+      }
 #pragma unroll
-        for (int o = 1; o < LPR; o <<= 1) d += __shfl_xor(d, o);
-        if (!live[uu]) continue;  // uniform within the row group
-        const float x = d * a.sc;
-        const float mm = fmaxf(m[g], x);
-        const float f = __builtin_amdgcn_exp2f(m[g] - mm);
-        const float p = __builtin_amdgcn_exp2f(x - mm);
+      for (int g = 0; g < G; ++g) {
+        // every lane takes part in the lane moves, masked rows included
+        const float dsum = group_sum<LPR>(x[g]);
+        x[g] = live[uu] ? dsum * a.sc : -INFINITY;
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        // online softmax; a masked row (x = -inf) leaves the state as it is
+        const float mm = fmaxf(m[g], x[g]);
+        const float f = m[g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[g] - mm);
+        const float p = x[g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(x[g] - mm);
         l[g] = l[g] * f + p;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e] * f);
@@ -195,12 +219,44 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial(DecArgs a) {
   }
 }
 
+// Chunk states are read in batches of kDecBatch with every load of a batch in
+// flight at once (the chunks were written by other XCDs, so each read is a
+// memory round trip): first the maximum, then the rescaled sums.
+constexpr int kDecBatch = 16;
+
 template <int D>
 __global__ __launch_bounds__(D) void decode_combine(DecArgs a) {
   const int j = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
   const float* pp = a.part + ((int64_t)b * a.HQ + j) * a.S * (D + 2);
-  float m = -INFINITY, l = 0.f, av = 0.f;
-  for (int s = 0; s < a.S; ++s) dec_merge(m, l, &av, pp[s * (D + 2)], pp[s * (D + 2) + 1], &pp[s * (D + 2) + 2 + e], 1);
+  float m = -INFINITY;
+  for (int s0 = 0; s0 < a.S; s0 += kDecBatch) {
+    float ms[kDecBatch];
+#pragma unroll
+    for (int i = 0; i < kDecBatch; ++i) ms[i] = s0 + i < a.S ? pp[(s0 + i) * (D + 2)] : -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kDecBatch; ++i) m = fmaxf(m, ms[i]);
+  }
+  float l = 0.f, av = 0.f;
+  if (m != -INFINITY) {
+    for (int s0 = 0; s0 < a.S; s0 += kDecBatch) {
+      float ms[kDecBatch], ls[kDecBatch], as[kDecBatch];
+#pragma unroll
+      for (int i = 0; i < kDecBatch; ++i) {
+        const bool ok = s0 + i < a.S;
+        const float* q = pp + (int64_t)(ok ? s0 + i : 0) * (D + 2);
+        ms[i] = ok ? q[0] : -INFINITY;
+        ls[i] = q[1];
+        as[i] = q[2 + e];
+      }
+#pragma unroll
+      for (int i = 0; i < kDecBatch; ++i) {
+        // empty chunks (m = -inf) weigh exp2(-inf) = 0
+        const float f = __builtin_amdgcn_exp2f(ms[i] - m);
+        l = fmaf(ls[i], f, l);
+        av = fmaf(as[i], f, av);
+      }
+    }
+  }
   a.out[((int64_t)b * a.HQ + j) * D + e] = l > 0.f ? av / l : 0.f;
 }
 
