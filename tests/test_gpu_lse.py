@@ -104,3 +104,37 @@ def test_e2e_lse_batch2_o64(gpu_lib):
 def test_full_llama8b_32k_lse_sampled_layers(gpu_lib):
     """The benchmark's 32k workload through kvec_evict_model_lse."""
     _e2e(gpu_lib, synth.workload(2), check_layers=[0, 1, 31], lse=True)
+
+
+def test_e2e_lse_window_equals_extended(gpu_lib):
+    """O' = O: no extended-window stages in the given-lse pipeline."""
+    _e2e(gpu_lib, _small("e2e-lse-wn-eq-o", 1800, 16, 16, 4, 2, 64, "bf16", B=120, layers=3),
+         lse=True)
+
+
+def test_e2e_lse_group7_entropy(gpu_lib):
+    """GQA group 7 (the Qwen2.5-7B grouping) with the entropy criterion."""
+    _e2e(gpu_lib, _small("e2e-lse-g7-ent", 2600, 32, 64, 4, 7, 128, "bf16", B=256, layers=3,
+                         criterion="entropy"), lse=True)
+
+
+def test_lse_keep_everything_when_budget_covers(gpu_lib):
+    """T <= B: every token is kept; the row normalisers are required but unread."""
+    import torch
+    kv = gpu_lib
+    w = _small("lse-keep-all", 100, 8, 16, 2, 2, 64, "bf16", B=128, layers=2)
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(max(kv.kvec_workspace_size(cfg), 256), dtype=torch.uint8, device="cuda")
+    from kvec_testlib import model_tensors
+    q, k, v = model_tensors(w)
+    lse = torch.full((2, 1, 4, w.rows), float("nan"), dtype=torch.float32, device="cuda")
+    bits = torch.zeros((1, 2, 2), dtype=torch.int64, device="cuda")
+    idx = torch.empty((2, 1, 2, 128), dtype=torch.int32, device="cuda")
+    ko = torch.empty((2, 1, 2, 128, 64), dtype=k.dtype, device="cuda")
+    vo = torch.empty_like(ko)
+    kv.kvec_evict_model_lse(cfg, q, lse, k, v, bits, idx, ko, vo, ws)
+    torch.cuda.synchronize()
+    gi = idx.cpu().numpy()
+    assert np.all(gi[:, :, :, :100] == np.arange(100))
+    assert np.all(gi[:, :, :, 100:] == -1)
+    assert torch.equal(ko[:, :, :, :100], k)
