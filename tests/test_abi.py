@@ -164,3 +164,25 @@ def test_status_strings():
     for s in range(5):
         assert isinstance(kvec.status_string(s), str) and kvec.status_string(s)
     assert kvec.status_string(99) == "unknown status"
+
+
+def test_plain_c_client(tmp_path):
+    """include/kvec.h compiles as C99 and a C program linked against libkvec.so
+    runs the host-only calls (no GPU needed)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    kvec.load()
+    exe = tmp_path / "abi_check"
+    libdir = os.path.dirname(kvec.LIB_PATH)
+    cmd = [gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(ROOT, "include"), "-I", "/opt/rocm/include",
+           os.path.join(ROOT, "tests", "c", "abi_check.c"), "-L", libdir, "-lkvec",
+           f"-Wl,-rpath,{libdir}", "-o", str(exe)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    assert "abi_check: ok" in r.stdout
