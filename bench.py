@@ -176,6 +176,60 @@ def time_steps(hip, stream, run, steps: int, warmup: int):
     return durs, wall
 
 
+def stage_breakdown(hip, stream, w, cfg, q, k, v, ws, idx, ko, vo, args) -> None:
+    """Per-layer entry points of every layer in order, each call bracketed by
+    HIP events: the separate launches of the score passes, the selection and
+    the gather (the fused step overlaps them; this shows each one's rate)."""
+    import torch
+    L, b, H, HQ, T, d, B = (w.n_layers, w.batch, w.n_kv_heads, w.n_q_heads, w.seq_len,
+                            w.head_dim, w.budget)
+    es = 2 if w.dtype == "bf16" else 4
+    Tc = w.candidates
+    p = torch.empty((b, H, Tc), dtype=torch.float32, device=q.device)
+    pe = torch.empty_like(p)
+    imp = torch.empty((b, Tc), dtype=torch.float32, device=q.device)
+    bits = torch.zeros((b, L, (T + 63) // 64), dtype=torch.int64, device=q.device)
+    calls = {
+        "kvec_score": lambda l: kvec_mod().kvec_score(cfg, q[l], k[l], p, pe, imp, ws),
+        "kvec_select_cover": lambda l: kvec_mod().kvec_select_cover(cfg, l, p, pe, imp, bits,
+                                                                    idx[l], None, ws),
+        "kvec_compact": lambda l: kvec_mod().kvec_compact(cfg, k[l], v[l], idx[l], ko[l], vo[l]),
+    }
+    for _ in range(max(1, args.warmup)):
+        for l in range(L):
+            for fn in calls.values():
+                fn(l)
+    torch.cuda.synchronize()
+    evs = _events(hip, 2 * L * len(calls))
+    for l in range(L):
+        for i, fn in enumerate(calls.values()):
+            e = 2 * (l * len(calls) + i)
+            assert hip.hipEventRecord(evs[e], stream) == 0
+            fn(l)
+            assert hip.hipEventRecord(evs[e + 1], stream) == 0
+    torch.cuda.synchronize()
+    out = {}
+    # bytes each call must move at least: the keys once and the query window
+    # (scores), the scores and counts (selection), the kept rows read and
+    # written (gather)
+    need = {"kvec_score": b * (H * T * d * es + HQ * w.rows * d * es + (2 * H + 1) * Tc * 4),
+            "kvec_select_cover": b * ((2 * H + 1) * Tc * 4 + H * B * 4),
+            "kvec_compact": b * 4 * H * B * d * es}
+    for i, name in enumerate(calls):
+        us = [_elapsed(hip, evs[2 * (l * len(calls) + i)], evs[2 * (l * len(calls) + i) + 1]) * 1e3
+              for l in range(L)]
+        avg = sum(us) / len(us)
+        gbs = need[name] / (avg * 1e-6) / 1e9
+        out[name] = {"us_per_layer": round(avg, 2), "algorithmic_bytes": need[name],
+                     "achieved_GBps": round(gbs, 1), "hbm_frac": round(gbs / HBM_PEAK_GBS, 4)}
+    print(json.dumps({"workload": w.name, "mode": "per-layer entry points", "stages": out}))
+
+
+def kvec_mod():
+    from paper_2606_29563_amd import kvec
+    return kvec
+
+
 def copy_calibration(mib: int) -> None:
     """A plain device copy of known size, to scale the HBM byte counters."""
     import torch
@@ -200,6 +254,9 @@ def main():
                     help="model: kvec_evict_model only; lse: kvec_evict_model_lse only "
                          "(row normalisers from the prefill); both: the headline plus the "
                          "given-lse step as a second object")
+    ap.add_argument("--stages", action="store_true",
+                    help="instead of the step: the per-layer entry points (kvec_score, "
+                         "kvec_select_cover, kvec_compact) one by one, each timed on its own")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -246,6 +303,9 @@ def main():
 
     hip = _hip()
     stream = torch.cuda.current_stream().cuda_stream  # the library's stream
+    if args.stages:
+        stage_breakdown(hip, stream, w, cfg, q, k, v, ws, idx, ko, vo, args)
+        return
     es = 2 if w.dtype == "bf16" else 4
     # algorithmic bytes of the whole step: K read once, the Q window, the gather
     # (read and write of the kept K and V rows)
