@@ -207,6 +207,20 @@ kvec_status kvec_evict_model(const kvec_config* cfg,
  * (n_layers + 11; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);
 
+/* One layer, as kvec_evict_layer, with that layer's window-row normalisers
+ * from the caller: the call a model makes inside the prefill of layer l, right
+ * after its attention has produced them (Sec. 5.1).
+ *   lse          device, fp32 [batch][n_q_heads][O'], strides {batch, head},
+ *                rows contiguous (see kvec_score_lse).  Required even when
+ *                T <= B (then unread). */
+kvec_status kvec_evict_layer_lse(const kvec_config* cfg, int32_t layer,
+                                 const void* q_win, const int64_t q_strides[3],
+                                 const float* lse, const int64_t lse_strides[2],
+                                 const void* k, const int64_t k_strides[3],
+                                 const void* v, const int64_t v_strides[3],
+                                 uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
+                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* The whole prefill eviction step, as kvec_evict_model, with the window rows'
  * normalisers from the caller (K-VEC applied inside each layer's prefill,
  * Sec. 5.1; see kvec_score_lse for their definition).

@@ -292,11 +292,15 @@ kvec_status kvec_compact(const kvec_config* cfg, const void* k, const int64_t k_
   return dev(run_compact(g, 1, m, stream));
 }
 
-kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* q_win,
-                             const int64_t q_strides[3], const void* k, const int64_t k_strides[3],
-                             const void* v, const int64_t v_strides[3], uint64_t* cover_bits,
-                             int32_t* idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
-                             hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+kvec_status evict_layer(const kvec_config* cfg, int32_t layer, const void* q_win,
+                        const int64_t q_strides[3], const float* lse, const int64_t lse_strides[2],
+                        const void* k, const int64_t k_strides[3], const void* v,
+                        const int64_t v_strides[3], uint64_t* cover_bits, int32_t* idx,
+                        void* k_out, void* v_out, void* ws, size_t ws_bytes, hipStream_t stream) {
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
@@ -321,12 +325,42 @@ kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* 
   m.idx = idx;
   m.k_out = k_out;
   m.v_out = v_out;
+  m.lse = lse;
+  if (lse) {
+    m.ls[1] = lse_strides[0];
+    m.ls[2] = lse_strides[1];
+  }
   if (g.keep_all) {
     const hipError_t e = run_keep_all(g, layer, cover_bits, idx, stream);
     if (e != hipSuccess) return KVEC_ERR_DEVICE;
     return dev(run_compact(g, 1, m, stream));
   }
   return dev(run_evict_layer(g, layer, m, static_cast<char*>(ws), w, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+kvec_status kvec_evict_layer(const kvec_config* cfg, int32_t layer, const void* q_win,
+                             const int64_t q_strides[3], const void* k, const int64_t k_strides[3],
+                             const void* v, const int64_t v_strides[3], uint64_t* cover_bits,
+                             int32_t* idx, void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  return evict_layer(cfg, layer, q_win, q_strides, nullptr, nullptr, k, k_strides, v, v_strides,
+                     cover_bits, idx, k_out, v_out, ws, ws_bytes, stream);
+}
+
+kvec_status kvec_evict_layer_lse(const kvec_config* cfg, int32_t layer, const void* q_win,
+                                 const int64_t q_strides[3], const float* lse,
+                                 const int64_t lse_strides[2], const void* k,
+                                 const int64_t k_strides[3], const void* v,
+                                 const int64_t v_strides[3], uint64_t* cover_bits, int32_t* idx,
+                                 void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+  if (!lse_ok(lse, lse_strides, 2)) return KVEC_ERR_INVALID;
+  return evict_layer(cfg, layer, q_win, q_strides, lse, lse_strides, k, k_strides, v, v_strides,
+                     cover_bits, idx, k_out, v_out, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -87,6 +87,7 @@ _lib = None
 
 EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_score_lse", "kvec_select_cover",
            "kvec_compact", "kvec_evict_layer", "kvec_evict_model", "kvec_evict_model_lse",
+           "kvec_evict_layer_lse",
            "kvec_profile_points", "kvec_profile_points_lse", "kvec_coverage",
            "kvec_decode_workspace_size", "kvec_decode_attention", "kvec_status_string"]
 
@@ -111,6 +112,8 @@ def load() -> ctypes.CDLL:
     lib.kvec_evict_layer.argtypes = [P, i32, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp, sz, vp]
     lib.kvec_evict_model.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp, sz, vp,
                                      ctypes.POINTER(vp)]
+    lib.kvec_evict_layer_lse.argtypes = [P, i32, vp, I64x, vp, I64x, vp, I64x, vp, I64x, vp, vp,
+                                         vp, vp, vp, sz, vp]
     lib.kvec_evict_model_lse.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp,
                                          vp, sz, vp, ctypes.POINTER(vp)]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
@@ -226,6 +229,18 @@ def kvec_evict_model(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, ws
                                    _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream), ev),
            "kvec_evict_model")
+
+
+def kvec_evict_layer_lse(cfg: Config, layer: int, q_win, lse, k, v, cover_bits, idx, k_out, v_out,
+                         ws, stream=None) -> None:
+    """As kvec_evict_layer, with the layer's natural-log row normalisers lse fp32 [b][HQ][O']."""
+    c = cfg.c()
+    _check(load().kvec_evict_layer_lse(ctypes.byref(c), layer, _ptr(q_win), _strides(q_win, 3),
+                                       _ptr(lse), _lse_strides(lse, 2), _ptr(k), _strides(k, 3),
+                                       _ptr(v), _strides(v, 3), _ptr(cover_bits), _ptr(idx),
+                                       _ptr(k_out), _ptr(v_out), _ptr(ws),
+                                       ws.numel() * ws.element_size(), _stream(stream)),
+           "kvec_evict_layer_lse")
 
 
 def kvec_evict_model_lse(cfg: Config, q_win, lse, k, v, cover_bits, idx, k_out, v_out, ws,

@@ -122,6 +122,13 @@ def test_entry_points_reject_before_launch():
                                   fake, 1 << 40, None) == kvec.KVEC_ERR_INVALID
     assert lib.kvec_score_lse(ctypes.byref(c), fake, st3, fake, ls2, fake, ks3, fake, fake, fake,
                               fake, 16, None) == kvec.KVEC_ERR_WORKSPACE
+    vs3 = ks3
+    assert lib.kvec_evict_layer_lse(ctypes.byref(c), 0, fake, st3, None, ls2, fake, ks3, fake, vs3,
+                                    fake, fake, fake, fake, fake, 1 << 40,
+                                    None) == kvec.KVEC_ERR_INVALID
+    assert lib.kvec_evict_layer_lse(ctypes.byref(c), 32, fake, st3, fake, ls2, fake, ks3, fake,
+                                    vs3, fake, fake, fake, fake, fake, 1 << 40,
+                                    None) == kvec.KVEC_ERR_INVALID
     st4 = (ctypes.c_int64 * 4)(32 * 64 * 128, 32 * 64 * 128, 64 * 128, 128)
     ks4 = (ctypes.c_int64 * 4)(8 * 32768 * 128, 8 * 32768 * 128, 32768 * 128, 128)
     ls3 = (ctypes.c_int64 * 3)(32 * 64, 32 * 64, 64)

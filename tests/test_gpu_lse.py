@@ -138,3 +138,36 @@ def test_lse_keep_everything_when_budget_covers(gpu_lib):
     assert np.all(gi[:, :, :, :100] == np.arange(100))
     assert np.all(gi[:, :, :, 100:] == -1)
     assert torch.equal(ko[:, :, :, :100], k)
+
+
+def test_layer_lse_calls_match_model_step(gpu_lib):
+    """kvec_evict_layer_lse called layer by layer (as inside a prefill loop)
+    reproduces kvec_evict_model_lse exactly."""
+    import torch
+    from test_gpu_parity import oracle_lse_tensor
+    from kvec_testlib import model_tensors
+    kv = gpu_lib
+    w = _small("layerwise-lse", 3000, 32, 64, 4, 4, 128, "bf16", batch=2, B=256, layers=4)
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    q, k, v = model_tensors(w)
+    lse = oracle_lse_tensor(w)
+    L, H, B, T, d = w.n_layers, w.n_kv_heads, w.budget, w.seq_len, w.head_dim
+    W = (T + 63) // 64
+    bits_m = torch.empty((w.batch, L, W), dtype=torch.int64, device="cuda")
+    idx_m = torch.empty((L, w.batch, H, B), dtype=torch.int32, device="cuda")
+    ko_m = torch.empty((L, w.batch, H, B, d), dtype=k.dtype, device="cuda")
+    vo_m = torch.empty_like(ko_m)
+    kv.kvec_evict_model_lse(cfg, q, lse, k, v, bits_m, idx_m, ko_m, vo_m, ws)
+    bits_l = torch.zeros_like(bits_m)
+    idx_l = torch.empty_like(idx_m)
+    ko_l = torch.empty_like(ko_m)
+    vo_l = torch.empty_like(vo_m)
+    for l in range(L):
+        kv.kvec_evict_layer_lse(cfg, l, q[l], lse[l], k[l], v[l], bits_l, idx_l[l], ko_l[l],
+                                vo_l[l], ws)
+    torch.cuda.synchronize()
+    assert torch.equal(idx_m, idx_l)
+    assert torch.equal(bits_m, bits_l)
+    assert torch.equal(ko_m.view(torch.int16), ko_l.view(torch.int16))
+    assert torch.equal(vo_m.view(torch.int16), vo_l.view(torch.int16))
