@@ -204,7 +204,7 @@ kvec_status kvec_evict_model(const kvec_config* cfg,
                              hipEvent_t* events);
 
 /* Number of events kvec_evict_model records when given an event array
- * (n_layers + 11; 0 when T <= B), or -1 for an invalid configuration. */
+ * (n_layers + 12; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);
 
 /* One layer, as kvec_evict_layer, with that layer's window-row normalisers
@@ -238,7 +238,7 @@ kvec_status kvec_evict_model_lse(const kvec_config* cfg,
                                  void* ws, size_t ws_bytes, hipStream_t stream,
                                  hipEvent_t* events);
 
-/* Number of events kvec_evict_model_lse records (n_layers + 7; 0 when
+/* Number of events kvec_evict_model_lse records (n_layers + 8; 0 when
  * T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points_lse(const kvec_config* cfg);
 

@@ -10,8 +10,8 @@
 namespace kvec {
 
 constexpr int kThreads = 512;  // every work-group of the step kernel: 8 waves
-constexpr int kPipeDepth = 10;         // launches between a layer's first and last stage
-constexpr int kPipeDepthLse = 6;       // the same when the row normalisers are given
+constexpr int kPipeDepth = 11;         // launches between a layer's first and last stage
+constexpr int kPipeDepthLse = 7;       // the same when the row normalisers are given
 constexpr int kRing = kPipeDepth + 1;  // layers in flight in the software pipeline
 
 constexpr int kTile1 = 512;       // keys per pass-1 work-group

@@ -8,8 +8,9 @@
 // Launch j of the step therefore runs, side by side in one grid of 512-thread
 // work-groups:
 //
-//   select   layer j-9   (one work-group per (sequence, head); the serial chain)
-//   count    layer j-9   (running coverage counts for the next selection)
+//   select B layer j-10  (one work-group per (sequence, head); the serial chain)
+//   count    layer j-10  (running coverage counts for the next selection)
+//   select A layer j-9   (members and preserve set; no earlier layer needed)
 //   pass 2   layer j-2   last-O rows, every head: P, I
 //   pass 2   layer j-6   extended rows, H_top heads: the rest of P over O'
 //   pass 1   layer j     last-O rows: row-normaliser partials
@@ -18,17 +19,18 @@
 //   pool     layer j-3   P: max-pool, sigma sums, histogram, I
 //   pool     layer j-7   P over O' of the H_top heads
 //   prep     layer j-8   (sigma, H_top, candidate members)
-//   gather   layer j-10  (compacted cache)
+//   gather   layer j-11  (compacted cache)
 //
-// so L + 10 launches cover the whole step and the serial selection chain
+// so L + 11 launches cover the whole step and the serial selection chain
 // runs in the shadow of the score passes.  Per-layer scratch lives in a ring
 // of kRing slots.
 //
 // When the caller supplies the window rows' normalisers (the log-sum-exp its
 // prefill attention already computed for those query rows), pass 1 and the
-// lse stages drop out and the step takes L + 6 launches: pass 2 of the
+// lse stages drop out and the step takes L + 7 launches: pass 2 of the
 // last-O rows at j, their pool at j-1, pass 2 of the extended rows at j-2,
-// their pool at j-3, prep at j-4, select and count at j-5, gather at j-6.
+// their pool at j-3, prep at j-4, select A at j-5, select B and count at
+// j-6, gather at j-7.
 //
 // Work-group IDs are dispatched round-robin over the 8 XCDs, each with its
 // own L2.  Within a stage, consecutive tasks (e.g. the row tiles of one key
@@ -108,7 +110,8 @@ __global__ void coverage_kernel(const uint64_t* bits, int64_t* count, int L, int
 int seg_count(const Problem& P, int st) {
   const bool ext = P.delta_eff > 0;
   switch (st) {
-    case ST_SELECT: return P.batch * P.H;
+    case ST_SELECT:
+    case ST_SELA: return P.batch * P.H;
     case ST_COUNT: return P.batch * ((P.words + kCountWords - 1) / kCountWords);
     case ST_PASS1: return P.batch * P.n_kt1 * P.n_rtg;
     case ST_P1B: return P.batch * P.n_kt1 * P.n_rtg_base;
@@ -226,9 +229,10 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
       set_seg(a, ST_P2X, j - 2);
       set_seg(a, ST_POOLX, j - 3);
       set_seg(a, ST_PREP, j - 4);
-      set_seg(a, ST_SELECT, j - 5);
-      set_seg(a, ST_COUNT, j - 5);
-      set_seg(a, ST_GATHER, j - 6);
+      set_seg(a, ST_SELA, j - 5);
+      set_seg(a, ST_SELECT, j - 6);
+      set_seg(a, ST_COUNT, j - 6);
+      set_seg(a, ST_GATHER, j - 7);
       if (ev) (void)hipEventRecord(ev[j], s);
       if ((e = launch(a, w, s)) != hipSuccess) return e;
     }
@@ -246,9 +250,10 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
     set_seg(a, ST_P2X, j - 6);
     set_seg(a, ST_POOLX, j - 7);
     set_seg(a, ST_PREP, j - 8);
-    set_seg(a, ST_SELECT, j - 9);
-    set_seg(a, ST_COUNT, j - 9);
-    set_seg(a, ST_GATHER, j - 10);
+    set_seg(a, ST_SELA, j - 9);
+    set_seg(a, ST_SELECT, j - 10);
+    set_seg(a, ST_COUNT, j - 10);
+    set_seg(a, ST_GATHER, j - 11);
     if (ev) (void)hipEventRecord(ev[j], s);
     if ((e = launch(a, w, s)) != hipSuccess) return e;
   }
@@ -304,8 +309,8 @@ static hipError_t select_stages(const Geometry& g, int layer, const float* p_raw
   a.idx = idx;
   a.htop = htop;
   a.standalone_counts = 1;
-  const int order[3] = {ST_POOL, ST_PREP, ST_SELECT};
-  for (int i = 0; i < 3; ++i) {
+  const int order[4] = {ST_POOL, ST_PREP, ST_SELA, ST_SELECT};
+  for (int i = 0; i < 4; ++i) {
     for (int st = 0; st < ST_N; ++st) a.seg[st] = Seg{-1, 0, 0};
     a.seg[order[i]] = Seg{layer, 0, seg_count(P, order[i])};
     if ((e = launch(a, w, s)) != hipSuccess) return e;

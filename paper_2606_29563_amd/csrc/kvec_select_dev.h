@@ -8,12 +8,15 @@
 //             head's selected score P_sel; then, from the histogram, a
 //             coverage-independent superset ("members") of every token that
 //             can be preserved or finally kept, in ascending token order.
-//   select    per (layer, sequence, head), run in layer order: the preserve
-//             set = first K tokens by (P_sel desc, t asc) (Sec. 4.2),
-//             P' = P_sel + lambda * I * (1 - n_t/(l+1)) in fp32 with one
-//             rounding per operation and P' = 1 on the preserve set, the first
-//             B-O by (P' desc, t asc) emitted in ascending order then the
-//             window, and the kept tokens OR-ed into the layer's bitmap row.
+//   select A  per (layer, sequence, head): the members in ascending order and
+//             the preserve set = first K tokens by (P_sel desc, t asc)
+//             (Sec. 4.2); needs nothing of the earlier layers.
+//   select B  per (layer, sequence, head), run in layer order, one launch
+//             after select A: P' = P_sel + lambda * I * (1 - n_t/(l+1)) in
+//             fp32 with one rounding per operation and P' = 1 on the preserve
+//             set, the first B-O by (P' desc, t asc) emitted in ascending order
+//             then the window, and the kept tokens OR-ed into the layer's
+//             bitmap row.
 //   count     the running coverage counts n_t of the pipeline.
 //
 // Why the superset is exact: for a non-preserved token, 0 <= bonus <=
@@ -397,14 +400,24 @@ __device__ __forceinline__ void block_flags(const uint32_t* kb, int n, int want,
   }
 }
 
-__device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io, int layer, int b,
-                                            int h, char* smem) {
+// The selection of a layer runs as two tasks one launch apart, both one
+// work-group per (sequence, head).  Only the second needs the previous
+// layer's bitmap row (n_t), so the first runs while that row is still being
+// written, which halves the serial chain from layer to layer.
+//
+// select A: gathers the head's candidate members (contiguous, ascending t),
+// takes the preserve set (first Kp by P_sel desc, t asc) and writes the
+// members back compacted into the head's member arrays: t (bitwise
+// complemented for preserved members), P_sel, I; their count goes to
+// mem_n[.][h][0].
+__device__ __forceinline__ void task_select_a(const Problem& P, const SelectIO& io, int b, int h,
+                                              char* smem) {
   uint32_t* hist = reinterpret_cast<uint32_t*>(smem);    // [2048]
   int* tmp = reinterpret_cast<int*>(hist + 2048);          // [32]
   int* off = tmp + 32;                                     // [n_prep + 1] member offsets
   char* marr = reinterpret_cast<char*>(off + ((P.n_prep + 1 + 3) & ~3));
   const int64_t hb = (int64_t)b * P.H + h;
-  const int32_t* mn = io.mem_n + hb * P.n_prep;
+  int32_t* mn = io.mem_n + hb * P.n_prep;
   // member offsets of the prep chunks (wave 0, 64 chunks per round)
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
@@ -437,9 +450,9 @@ __device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io
   // gather the members contiguously (ascending t), with their preserve keys;
   // kBatch members per thread have their loads in flight together
   constexpr int kBatch = 8;
-  const int32_t* gt = io.mem_t + hb * P.Tc;
-  const float* gp = io.mem_ps + hb * P.Tc;
-  const float* gi = io.mem_i + hb * P.Tc;
+  int32_t* gt = io.mem_t + hb * P.Tc;
+  float* gp = io.mem_ps + hb * P.Tc;
+  float* gi = io.mem_i + hb * P.Tc;
   for (int i0 = threadIdx.x; i0 < n; i0 += kBatch * blockDim.x) {
     int g[kBatch];  // member position in the head's chunk arrays
 #pragma unroll
@@ -473,31 +486,102 @@ __device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io
     }
   }
   __syncthreads();
-  // 1. preserve set: first Kp members by (P_sel desc, t asc)
+  // preserve set: first Kp members by (P_sel desc, t asc)
   const int kp = min(P.Kp, n);
   uint32_t thr_p = 0xffffffffu;
   int take_p = 0;
   if (kp > 0 && kp < n) block_radix_select(kb, n, kp, hist, tmp, thr_p, take_p);
-  // 2. P' keys: 1.0 on the preserve set, else P_sel + lambda * I * (1 - n_t/(l+1))
+  // write the members back compacted (every chunk-layout read is done: the
+  // gather ended with a barrier), preserved ones marked by ~t
+  block_flags(kb, n, kp, thr_p, take_p, tmp, [&](int i, bool pres) {
+    gt[i] = pres ? ~mt[i] : mt[i];
+    gp[i] = mp[i];
+    gi[i] = mi[i];
+  });
+  if (threadIdx.x == 0) mn[0] = n;
+}
+
+// select B: the coverage-aware priority P' of every member (1.0 on the
+// preserve set, else P_sel + lambda * I * (1 - n_t/(l+1)) in fp32 op by op),
+// the final pick of the first B-O by (P' desc, t asc), its emission in
+// ascending order with the window, and the layer's bitmap row.
+__device__ __forceinline__ void task_select_b(const Problem& P, const SelectIO& io, int layer, int b,
+                                              int h, char* smem) {
+  uint32_t* hist = reinterpret_cast<uint32_t*>(smem);    // [2048]
+  int* tmp = reinterpret_cast<int*>(hist + 2048);          // [32]
+  char* marr = reinterpret_cast<char*>(tmp + 32 + ((P.n_prep + 1 + 3) & ~3));
+  const int64_t hb = (int64_t)b * P.H + h;
+  const int n = io.mem_n[hb * P.n_prep];
+  const int32_t* gt = io.mem_t + hb * P.Tc;
+  const float* gp = io.mem_ps + hb * P.Tc;
+  const float* gi = io.mem_i + hb * P.Tc;
+  uint32_t* kb;
+  const int32_t* mt;
+  const float *mp, *mi;
+  if (n <= P.mcap) {
+    kb = reinterpret_cast<uint32_t*>(marr);
+    int32_t* lt = reinterpret_cast<int32_t*>(kb + P.mcap);
+    float* lp = reinterpret_cast<float*>(lt + P.mcap);
+    float* li = lp + P.mcap;
+    // members into LDS, kBatch loads per thread in flight together
+    constexpr int kBatch = 8;
+    for (int i0 = threadIdx.x; i0 < n; i0 += kBatch * blockDim.x) {
+      int32_t vt[kBatch];
+      float vp[kBatch], vi[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = min(i0 + u * (int)blockDim.x, n - 1);
+        vt[u] = gt[i];
+        vp[u] = gp[i];
+        vi[u] = gi[i];
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int i = i0 + u * (int)blockDim.x;
+        if (i < n) {
+          lt[i] = vt[u];
+          lp[i] = vp[u];
+          li[i] = vi[u];
+        }
+      }
+    }
+    __syncthreads();
+    mt = lt;
+    mp = lp;
+    mi = li;
+  } else {
+    // long member lists stay in global memory; the keys go to this layer's
+    // pooled-score array, free once the candidates were extracted
+    kb = reinterpret_cast<uint32_t*>(io.pooled) + hb * P.Tc;
+    mt = gt;
+    mp = gp;
+    mi = gi;
+  }
+  // P' keys: 1.0 on the preserve set, else P_sel + lambda * I * (1 - n_t/(l+1))
   const float f_denom = (float)(layer + 1);
   const uint8_t* cnt = io.cnt_in;
   const uint64_t* prow = io.bits_prev;
-  block_flags(kb, n, kp, thr_p, take_p, tmp, [&](int i, bool pres) {
-    float pp;
-    if (pres) {
-      pp = 1.0f;
-    } else {
-      const int t = mt[i];
-      int nt = cnt ? (int)cnt[(int64_t)b * P.T + t] : 0;
-      if (prow) nt += (int)((prow[(int64_t)b * P.L * P.words + (t >> 6)] >> (t & 63)) & 1ull);
-      const float cov = __fdiv_rn((float)nt, f_denom);
-      const float focus = __fmul_rn(mi[i], __fsub_rn(1.0f, cov));
-      pp = __fadd_rn(mp[i], __fmul_rn(P.lam, focus));
+  {
+    const int per = (n + blockDim.x - 1) / blockDim.x;
+    const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
+    for (int i = lo; i < hi; ++i) {
+      const int te = mt[i];
+      float pp;
+      if (te < 0) {
+        pp = 1.0f;
+      } else {
+        const int t = te;
+        int nt = cnt ? (int)cnt[(int64_t)b * P.T + t] : 0;
+        if (prow) nt += (int)((prow[(int64_t)b * P.L * P.words + (t >> 6)] >> (t & 63)) & 1ull);
+        const float cov = __fdiv_rn((float)nt, f_denom);
+        const float focus = __fmul_rn(mi[i], __fsub_rn(1.0f, cov));
+        pp = __fadd_rn(mp[i], __fmul_rn(P.lam, focus));
+      }
+      kb[i] = float_key(pp);
     }
-    kb[i] = float_key(pp);
-  });
+  }
   __syncthreads();
-  // 3. final pick: first M members by (P' desc, t asc), emitted in ascending order
+  // final pick: first M members by (P' desc, t asc), emitted in ascending order
   const int m = min(P.M, n);
   uint32_t thr = 0xffffffffu;
   int take = 0;
@@ -531,7 +615,8 @@ __device__ __forceinline__ void task_select(const Problem& P, const SelectIO& io
     int e = e0;
     for (int i = lo; i < hi; ++i) {
       if (!selected(kb[i], e)) continue;
-      const int t = mt[i];
+      const int te = mt[i];
+      const int t = te < 0 ? ~te : te;
       out[o++] = t;
       if ((t >> 6) != cur) {
         if (cur >= 0) atomicOr((unsigned long long*)&row[cur], (unsigned long long)word);

@@ -16,7 +16,7 @@ namespace step {
 // *_X are the last-O and the extended-window halves of the layer pipeline;
 // the plain stages cover every row and head (per-layer entry points).
 enum Stage {
-  ST_SELECT = 0, ST_COUNT,
+  ST_SELECT = 0, ST_SELA, ST_COUNT,
   ST_PASS2, ST_P2B, ST_P2X,
   ST_PASS1, ST_P1B, ST_P1X,
   ST_LSE, ST_LSEB, ST_LSEX,
@@ -187,7 +187,12 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
   switch (st) {
     case ST_SELECT: {
       const int b = blk / P.H, h = blk % P.H;
-      task_select(P, select_io(a, sg.layer, sg.slot), sg.layer, b, h, smem);
+      task_select_b(P, select_io(a, sg.layer, sg.slot), sg.layer, b, h, smem);
+      break;
+    }
+    case ST_SELA: {
+      const int b = blk / P.H, h = blk % P.H;
+      task_select_a(P, select_io(a, sg.layer, sg.slot), b, h, smem);
       break;
     }
     case ST_COUNT: {

@@ -36,8 +36,8 @@ int main(void) {
   size_t ws = 0, dws = 0;
   CHECK(kvec_workspace_size(&c, &ws) == KVEC_OK && ws > 0);
   CHECK(kvec_decode_workspace_size(&c, 1024, &dws) == KVEC_OK && dws > 0);
-  CHECK(kvec_profile_points(&c) == 32 + 11);
-  CHECK(kvec_profile_points_lse(&c) == 32 + 7);
+  CHECK(kvec_profile_points(&c) == 32 + 12);
+  CHECK(kvec_profile_points_lse(&c) == 32 + 8);
 
   /* validation happens before any launch: bad configurations and null
    * pointers come back as statuses, with no device touched */

@@ -161,8 +161,8 @@ def test_decode_validation():
 
 
 def test_profile_points():
-    assert kvec.kvec_profile_points(_cfg()) == 32 + 11
-    assert kvec.kvec_profile_points_lse(_cfg()) == 32 + 7
+    assert kvec.kvec_profile_points(_cfg()) == 32 + 12
+    assert kvec.kvec_profile_points_lse(_cfg()) == 32 + 8
     assert kvec.kvec_profile_points_lse(_cfg(seq_len=512, budget=1024)) == 0
     assert kvec.kvec_profile_points_lse(_cfg(batch=0)) == -1
 
