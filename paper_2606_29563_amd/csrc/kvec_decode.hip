@@ -11,7 +11,7 @@
 //   partial  one work-group per (row chunk, KV head, sequence): the G query
 //            heads of the KV head share every K/V row read.  A row is read by
 //            a group of lanes, 16 bytes each (fully coalesced), the group's
-//            partial dot products are summed with lane shuffles, and each
+//            partial dot products are summed with DPP lane moves, and each
 //            lane keeps an online-softmax state (max, sum, weighted V
 //            elements) per query head.  States merge across the row groups
 //            of a wave by shuffles, across waves through LDS, and the
