@@ -66,11 +66,18 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   x.nsum = x.O % x.WR == 0 ? 1 : 2;
   const int tpw = 8 / H;
   x.n_rtg = (x.n_rt + tpw - 1) / tpw;
-  x.n_kt1 = (x.T + kTile1 - 1) / kTile1;
+  // Keys per score work-group: 512 from T = 16384 on, smaller for shorter
+  // prefixes (at least 128) so that their launches fill more CUs with
+  // shorter work-groups: the largest power of two <= T / 32 in [128, 512].
+  int tile_target = kTileMax;
+  while (tile_target > kTileMin && tile_target * 32 > x.T) tile_target /= 2;
+  x.tile1 = tile_target;
+  x.n_kt1 = (x.T + x.tile1 - 1) / x.tile1;
   // pass-2 LDS: the key ring plus, per row tile, the running max over heads
   // (SK keys per exchange period), the staged per-key sums and importance of
-  // the key tile.  Prefer 512-key tiles (fewer work-groups, less fixed cost
-  // per key) with periods of at least 32 keys, then the widest period.
+  // the key tile.  Prefer the target tile (fewer work-groups, less fixed
+  // cost per key) with periods of at least 32 keys at 512, then the widest
+  // period; halve the tile only when the LDS budget requires it.
   const size_t ring = key_ring_bytes(c->dtype == KVEC_BF16 ? 2 : 4, x.D);
   // row tiles of the layer pipeline: the last-O rows for every head, the
   // remaining extended-window rows for the delta_eff heads of H_top
@@ -86,8 +93,8 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   };
   const size_t lds_cap = kLdsMax - kLdsStatic;
   x.tile2 = 0;
-  for (int tile = kTile2Max; tile >= kTile2Max / 2 && !x.tile2; tile /= 2)
-    for (int sk = tile; sk >= (tile == kTile2Max ? 32 : 16); sk = sk == tile ? 128 : sk / 2)
+  for (int tile = tile_target; tile >= kTileMin && !x.tile2; tile /= 2)
+    for (int sk = tile; sk >= (tile == kTileMax ? 32 : 16); sk = (sk == tile && tile > 128) ? 128 : sk / 2)
       if (lds_p2(sk, tile) <= lds_cap) {
         x.tile2 = tile;
         x.SK = sk;  // a power of two

@@ -14,8 +14,8 @@ constexpr int kPipeDepth = 11;         // launches between a layer's first and l
 constexpr int kPipeDepthLse = 7;       // the same when the row normalisers are given
 constexpr int kRing = kPipeDepth + 1;  // layers in flight in the software pipeline
 
-constexpr int kTile1 = 512;       // keys per pass-1 work-group
-constexpr int kTile2Max = 512;    // keys per pass-2 work-group (512 or 256, by LDS)
+constexpr int kTileMax = 512;     // keys per score work-group at long prefixes
+constexpr int kTileMin = 128;     // ... and the least at short ones
 constexpr int kPoolChunk = 512;   // tokens per pool statistics entry (one wave)
 constexpr int kPrepChunk = 1024;  // tokens per candidate chunk (one wave, 16 per lane)
 constexpr int kPoolPer = 8;       // pool chunks per pool work-group (one per wave)
@@ -65,7 +65,7 @@ enum Part { PART_ALL = 0, PART_BASE = 1, PART_EXT = 2 };
 struct Problem {
   int batch, L, H, HQ, G, D, T, O, Wn, Tc, B, M, Kp, pool, delta_eff;
   float lam, sc, inv_go, inv_gwn;
-  int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK, tile2;
+  int WR, n_rt, n_rt_base, n_rtg, n_kt1, n_kt2, SK, tile1, tile2;
   int sk_shift;    // log2(SK): exchange periods are powers of two
   int nsum;        // pass-2 per-key sums per head: 1 when O is a multiple of WR (no row
                    // tile holds both last-O and earlier rows), else 2

@@ -354,7 +354,7 @@ struct ScoreTile {
       for (int i = 0; i < 4; ++i) pos[rb][i] = P.T - P.Wn + (r_lo + rb * 16 + 4 * c + i);
 
     tend = PASS == 1 ? P.T : P.Tc;
-    const int tile = PASS == 1 ? kTile1 : P.tile2;
+    const int tile = PASS == 1 ? P.tile1 : P.tile2;
     ks = kt * tile;
     ke = min(ks + tile, tend);
     lim_min = P.T - P.Wn + max(r_lo, 0);
@@ -798,8 +798,8 @@ __device__ __noinline__ float2 lse_partial_exact(const Problem P, const char* q,
     }
   }
   float m = -INFINITY, l = 0.f;
-  const int t1 = min((kt + 1) * kTile1, min(P.T, pos + 1));
-  for (int t = kt * kTile1; t < t1; ++t) {
+  const int t1 = min((kt + 1) * P.tile1, min(P.T, pos + 1));
+  for (int t = kt * P.tile1; t < t1; ++t) {
     const char* kr = k + (kb + (int64_t)t * ks_t) * ES;
     float dot = 0.f;
     for (int i = 0; i < D; ++i) {
