@@ -41,6 +41,8 @@ SCORE_CASES = [
     _small("bf16-d64-g2-short", 70, 16, 64, 2, 2, 64, "bf16"),
     _small("f32-d128-g1", 200, 8, 8, 2, 1, 128, "f32"),
     _small("bf16-d128-g4-wn-eq-o", 600, 32, 32, 4, 4, 128, "bf16"),
+    # the longest supported prefix (T = 2^18), one KV head
+    _small("bf16-d64-g1-max-T", 1 << 18, 32, 64, 1, 1, 64, "bf16", B=2048),
     # key tiles of 256 (8192 <= T < 16384; shorter prefixes use 128, longer 512)
     _small("bf16-d128-g4-tile256", 9000, 32, 64, 8, 4, 128, "bf16"),
     # group sizes that are not powers of two (Qwen2.5: 7 for 7B, 5 for 14B/32B, 6 for 1.5B)
@@ -253,6 +255,11 @@ def test_e2e_tiny_fp32(gpu_lib):
 
 def test_e2e_small_bf16(gpu_lib):
     _e2e(gpu_lib, _small("e2e-small", 2500, 32, 64, 8, 4, 128, "bf16", B=200, layers=6))
+
+
+def test_e2e_max_prefix(gpu_lib):
+    """The longest supported prefix, T = 2^18, two KV heads of group 2."""
+    _e2e(gpu_lib, _small("e2e-max-T", 1 << 18, 32, 64, 2, 2, 64, "bf16", B=2048, layers=2))
 
 
 def test_e2e_tile256_bf16(gpu_lib):
