@@ -81,8 +81,13 @@ def cpu_baseline(w, max_layers: int, min_seconds: float = 10.0):
         done += 1
     per_layer = t_work / done
     step_s = per_layer * w.n_layers * w.batch
-    threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
-    return {"value": w.batch * w.seq_len / step_s, "unit": "prefix tokens/s", "cores": threads,
+    # the oracle's only parallel part is numpy's BLAS (the window products):
+    # the threads it used are that pool's size, at most the CPUs this process
+    # may run on
+    blas = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    host = len(os.sched_getaffinity(0))
+    return {"value": w.batch * w.seq_len / step_s, "unit": "prefix tokens/s",
+            "cores": min(blas, host), "blas_threads": blas, "host_cpus": host,
             "kind": "oracle",
             "sample": f"{done} layer evictions of sequence 0 in layer order ({t_work:.1f} s of "
                       f"oracle work, input generation excluded); per-layer time extrapolated "
@@ -323,11 +328,20 @@ def main():
     step_flops = 2 * d * L * b * (HQ * O * T + (HQ // H) * delta * (Wn - O) * T)
 
     def mfma(ms_step_gpu, passes):
-        tf = step_flops * passes / (ms_step_gpu * 1e-3) / 1e12
+        # frac: the method's own matrix work (one product per logit) over the
+        # step time; executed_*: what the kernel runs (one product per score
+        # pass, two when the row normalisers are computed here)
+        tf = step_flops / (ms_step_gpu * 1e-3) / 1e12
+        tx = step_flops * passes / (ms_step_gpu * 1e-3) / 1e12
         return {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                "flops_per_step": step_flops * passes,
-                "note": f"{passes} score pass(es) over those rows; dense bf16 peak"}
+                "flops_per_step": step_flops,
+                "executed_passes": passes, "executed_flops_per_step": step_flops * passes,
+                "executed_achieved": round(tx, 1),
+                "executed_frac": round(tx / MFMA_BF16_PEAK_TFLOPS, 4),
+                "note": "algorithmic flops: one q.k product per logit of the last-O rows of "
+                        "every query head and of the extended rows of the H_top heads; dense "
+                        "bf16 peak"}
 
     def roofline(durs, n_launch, traffic):
         # Average duration of a fused launch: each step's interval between HIP

@@ -91,7 +91,7 @@ typedef enum kvec_dtype {
 /* Shape and hyper-parameters of one eviction problem (Algorithm 1 inputs). */
 typedef struct kvec_config {
   int32_t batch;          /* independent sequences, >= 1 */
-  int32_t n_layers;       /* L, >= 1 (rows of the coverage bitmap) */
+  int32_t n_layers;       /* L, 1..255 (rows of the coverage bitmap; n_t is kept in 8 bits) */
   int32_t n_kv_heads;     /* H in {1, 2, 4, 8} */
   int32_t n_q_heads;      /* multiple of H; G = n_q_heads / H in 1..8 */
   int32_t head_dim;       /* d in {64, 128} */

@@ -609,6 +609,66 @@ def test_coverage_is_union_size():
     assert n_t.max() <= 3
 
 
+def check_counts_hand(counts_from_bits):
+    """n_t (Sec. 4.2: the number of earlier layers that kept token t, the coverage
+    counters of Algorithm 1), counted by hand over four known layer bitmaps."""
+    rows = [np.array(r, dtype=bool) for r in (
+        [1, 0, 1, 0, 1, 0, 0, 1, 0, 1],
+        [1, 1, 0, 0, 1, 0, 0, 1, 0, 0],
+        [0, 1, 0, 0, 1, 0, 1, 1, 0, 0],
+        [1, 0, 0, 1, 1, 0, 0, 1, 0, 1])]
+    # column totals written out by hand, not computed
+    assert list(counts_from_bits(rows[:1])) == [1, 0, 1, 0, 1, 0, 0, 1, 0, 1]
+    assert list(counts_from_bits(rows[:2])) == [2, 1, 1, 0, 2, 0, 0, 2, 0, 1]
+    assert list(counts_from_bits(rows[:3])) == [2, 2, 1, 0, 3, 0, 1, 3, 0, 1]
+    assert list(counts_from_bits(rows)) == [3, 2, 1, 1, 4, 0, 1, 4, 0, 2]
+
+
+def test_counts_hand():
+    check_counts_hand(orc.counts_from_bits)
+
+
+def test_counts_from_kept_indices():
+    """n_t from layer_bits of index sets: a token kept by two heads of one layer
+    counts once for that layer; the window counts in every layer."""
+    T = 12
+    l0 = np.array([[0, 3, 10, 11], [3, 5, 10, 11]], dtype=np.int32)   # t = 3 kept by both heads
+    l1 = np.array([[1, 3, 10, 11], [2, 7, 10, 11]], dtype=np.int32)
+    n_t = orc.counts_from_bits([orc.layer_bits(l0, T), orc.layer_bits(l1, T)])
+    assert list(n_t) == [1, 1, 1, 2, 0, 1, 0, 1, 0, 0, 2, 2]
+
+
+def check_pool_before_sigma(select_layer):
+    """Pooling comes before sigma, and the H_top heads take the POOLED P over O'.
+
+    Head 0's raw P alternates 0.02 / 0: a large raw sigma, but max-pooling with
+    kernel 3 makes it exactly flat (pooled sigma 0).  Head 1 is a smooth step
+    (raw sigma 0.002).  With delta = 1, sigma of pooled P picks head 0; sigma of
+    raw P would pick head 1.  Head 0's P over O' has one spike at t = 30 and a
+    lower one at t = 5: pooled, the spike covers 29..31, so the three prefix picks
+    are 29, 30, 31; unpooled they would be 30, 5 and then 0 (a tie at the floor).
+    """
+    T, O, B = 42, 2, 5                   # Tc = 40, three prefix picks, preserve floor(1.25) = 1
+    Tc = T - O
+    p = np.zeros((2, Tc), np.float32)
+    p[0, ::2] = 0.02
+    p[1, :20], p[1, 20:] = 0.001, 0.005
+    pe = p.copy()
+    pe[0] = 0.001
+    pe[0, 30] = 0.5
+    pe[0, 5] = 0.1
+    imp = np.zeros(Tc, np.float32)
+    res = select_layer(p, pe, imp, np.zeros(T, int), 1, T=T, window=O, window_ext=4, budget=B,
+                       pool_kernel=3, delta=1, lam=0.0, beta=0.25)
+    assert list(res.htop) == [0]
+    assert list(res.idx[0, :3]) == [29, 30, 31]
+    assert res.keep[0, 29] and res.keep[0].sum() == 1
+
+
+def test_pool_before_sigma():
+    check_pool_before_sigma(orc.select_layer)
+
+
 def test_gather_rows():
     x = _rng(25).standard_normal((2, 10, 4))
     idx = np.array([[3, 1, 9, -1], [0, 0, 5, 2]], dtype=np.int32)
@@ -766,6 +826,64 @@ def _mut_preserve_raw(p_raw, p_ext_raw, imp, n_t, layer, **kw):
     return res
 
 
+def _mut_counts_or(layer_bits_list):
+    """Mistake: a token kept in any earlier layer counts once (OR instead of a sum)."""
+    u = np.zeros_like(np.asarray(layer_bits_list[0], dtype=bool))
+    for b in layer_bits_list:
+        u |= np.asarray(b, dtype=bool)
+    return u.astype(np.int64)
+
+
+def _mut_counts_last(layer_bits_list):
+    """Mistake: only the previous layer is counted."""
+    return np.asarray(layer_bits_list[-1], dtype=np.int64)
+
+
+def _select_variant(p_raw, p_ext_raw, imp, n_t, layer, *, sigma_raw=False, ext_unpooled=False,
+                    T, window, window_ext, budget, pool_kernel, delta, lam, beta):
+    """select_layer with one of two planted mistakes in the order of operations."""
+    O = window
+    Tc = T - O
+    H = p_raw.shape[0]
+    pooled = orc.maxpool1d(p_raw.astype(np.float32), pool_kernel)
+    pooled_ext = orc.maxpool1d(p_ext_raw.astype(np.float32), pool_kernel)
+    sig = orc.head_sigma(p_raw if sigma_raw else pooled)
+    htop = orc.adjusted_heads(sig, delta) if min(window_ext, T) > O else np.zeros(0, np.int64)
+    p_sel = pooled.copy()
+    p_sel[htop] = (p_ext_raw if ext_unpooled else pooled_ext)[htop]
+    kp = orc.preserve_count(budget, O, beta)
+    keep = np.zeros((H, Tc), dtype=bool)
+    for h in range(H):
+        keep[h, orc.rank_first(p_sel[h], kp)] = True
+    p_adj = orc.adjusted_priority(p_sel, imp, np.asarray(n_t)[:Tc], layer, lam, keep)
+    m = budget - O
+    idx = np.empty((H, budget), dtype=np.int32)
+    for h in range(H):
+        idx[h, :m] = np.sort(orc.rank_first(p_adj[h], m))
+        idx[h, m:] = np.arange(Tc, T)
+    return orc.LayerResult(idx, htop, sig, keep, p_sel, p_adj, np.zeros(T, bool))
+
+
+def _mut_sigma_raw(*a, **kw):
+    return _select_variant(*a, sigma_raw=True, **kw)
+
+
+def _mut_ext_unpooled(*a, **kw):
+    return _select_variant(*a, ext_unpooled=True, **kw)
+
+
+def test_select_variant_matches_oracle_without_mistakes():
+    """The mutation harness itself reproduces the oracle when no mistake is planted."""
+    H, T, O, B = 4, 300, 8, 40
+    p, pe, imp = _scores(31, H, T - O)
+    n_t = _rng(32).integers(0, 3, size=T)
+    kw = dict(T=T, window=O, window_ext=16, budget=B, pool_kernel=5, delta=2, lam=1.0, beta=0.25)
+    a = orc.select_layer(p, pe, imp, n_t, 3, **kw)
+    b = _select_variant(p, pe, imp, n_t, 3, **kw)
+    np.testing.assert_array_equal(a.idx, b.idx)
+    np.testing.assert_array_equal(a.htop, b.htop)
+
+
 @pytest.mark.parametrize("check,mutant", [
     (check_zero_query_closed_form, _mut_no_causal),
     (check_zero_query_closed_form, _mut_wrong_window),
@@ -789,6 +907,10 @@ def _mut_preserve_raw(p_raw, p_ext_raw, imp, n_t, layer, **kw):
     (check_rank_brute, _mut_rank_index_desc),
     (check_maxpool, _mut_maxpool_shift),
     (check_preserve_uses_replaced_scores, _mut_preserve_raw),
+    (check_counts_hand, _mut_counts_or),
+    (check_counts_hand, _mut_counts_last),
+    (check_pool_before_sigma, _mut_sigma_raw),
+    (check_pool_before_sigma, _mut_ext_unpooled),
 ])
 def test_pins_catch_planted_mistakes(check, mutant):
     with pytest.raises(AssertionError):
