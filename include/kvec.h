@@ -203,6 +203,30 @@ kvec_status kvec_evict_model(const kvec_config* cfg,
                              void* ws, size_t ws_bytes, hipStream_t stream,
                              hipEvent_t* events);
 
+/* The whole step, as kvec_evict_model, also handing out every layer's window
+ * scores as the pipeline computed them: P over the last O rows (Sec. 4.1,
+ * Eq. eviction), P over the extended window O' of the H_top heads (Sec. 4.1)
+ * and the global importance I (Sec. 4.2), all before pooling, and the H_top
+ * set of each layer.
+ *   p_raw_out   device out, fp32 [L][batch][H][T-O], contiguous.
+ *   p_ext_out   device out, fp32 [L][batch][H][T-O], contiguous; only the rows
+ *               of the heads in that layer's H_top are written (the pipeline
+ *               scores the extended window for those heads only), the others
+ *               are left as the caller set them.
+ *   imp_out     device out, fp32 [L][batch][T-O], contiguous.
+ *   htop_out    device out, uint32 [L][batch]: bit h set for h in H_top.
+ * All four are required and 4-byte aligned (else KVEC_ERR_INVALID).  When
+ * T <= B nothing is scored and they are left unchanged.  Other arguments,
+ * outputs and errors as kvec_evict_model (no profiling events). */
+kvec_status kvec_evict_model_scores(const kvec_config* cfg,
+                                    const void* q_win, const int64_t q_strides[4],
+                                    const void* k, const int64_t k_strides[4],
+                                    const void* v, const int64_t v_strides[4],
+                                    uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
+                                    float* p_raw_out, float* p_ext_out, float* imp_out,
+                                    uint32_t* htop_out, void* ws, size_t ws_bytes,
+                                    hipStream_t stream);
+
 /* Number of events kvec_evict_model records when given an event array
  * (n_layers + 12; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);

@@ -378,7 +378,8 @@ kvec_status evict_model(const kvec_config* cfg, const void* q_win, const int64_t
                         const float* lse, const int64_t lse_strides[3], const void* k,
                         const int64_t k_strides[4], const void* v, const int64_t v_strides[4],
                         uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out, void* ws,
-                        size_t ws_bytes, hipStream_t stream, hipEvent_t* events) {
+                        size_t ws_bytes, hipStream_t stream, hipEvent_t* events,
+                        const ModelIO* scores = nullptr) {
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
@@ -408,6 +409,12 @@ kvec_status evict_model(const kvec_config* cfg, const void* q_win, const int64_t
   m.lse = lse;
   if (lse)
     for (int i = 0; i < 3; ++i) m.ls[i] = lse_strides[i];
+  if (scores) {
+    m.sc_p = scores->sc_p;
+    m.sc_pe = scores->sc_pe;
+    m.sc_imp = scores->sc_imp;
+    m.sc_htop = scores->sc_htop;
+  }
   if (g.keep_all) {
     for (int l = 0; l < g.p.L; ++l) {
       const hipError_t e = run_keep_all(g, l, cover_bits, idx + (int64_t)l * g.p.batch * g.p.H * g.p.B,
@@ -442,6 +449,25 @@ kvec_status kvec_evict_model_lse(const kvec_config* cfg, const void* q_win,
   if (!lse_ok(lse, lse_strides, 3)) return KVEC_ERR_INVALID;
   return evict_model(cfg, q_win, q_strides, lse, lse_strides, k, k_strides, v, v_strides,
                      cover_bits, idx, k_out, v_out, ws, ws_bytes, stream, events);
+}
+
+kvec_status kvec_evict_model_scores(const kvec_config* cfg, const void* q_win,
+                                    const int64_t q_strides[4], const void* k,
+                                    const int64_t k_strides[4], const void* v,
+                                    const int64_t v_strides[4], uint64_t* cover_bits, int32_t* idx,
+                                    void* k_out, void* v_out, float* p_raw_out, float* p_ext_out,
+                                    float* imp_out, uint32_t* htop_out, void* ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  const auto f4 = [](const void* p) { return p && ((uintptr_t)p & 3u) == 0; };
+  if (!f4(p_raw_out) || !f4(p_ext_out) || !f4(imp_out) || !f4(htop_out)) return KVEC_ERR_INVALID;
+  ModelIO sc;
+  memset(&sc, 0, sizeof(sc));
+  sc.sc_p = p_raw_out;
+  sc.sc_pe = p_ext_out;
+  sc.sc_imp = imp_out;
+  sc.sc_htop = htop_out;
+  return evict_model(cfg, q_win, q_strides, nullptr, nullptr, k, k_strides, v, v_strides,
+                     cover_bits, idx, k_out, v_out, ws, ws_bytes, stream, nullptr, &sc);
 }
 
 kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, int32_t upto_layer,

@@ -110,6 +110,13 @@ struct ModelIO {
   void* v_out;
   const float* lse;       // nullable: natural-log row normalisers [layer][b][HQ][Wn], strides ls
   int64_t ls[3];
+  // nullable score outputs of the layer pipeline (all four or none): P and P
+  // over O' before pooling [layer][b][H][Tc] (P over O' for the H_top heads
+  // only), I [layer][b][Tc], H_top masks [layer][b]
+  float* sc_p;
+  float* sc_pe;
+  float* sc_imp;
+  uint32_t* sc_htop;
 };
 
 hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Workspace& w,

@@ -161,6 +161,10 @@ void set_model(StepArgs& a, const ModelIO& m) {
   a.idx = m.idx;
   a.k_out = static_cast<char*>(m.k_out);
   a.v_out = static_cast<char*>(m.v_out);
+  a.sc_p = m.sc_p;
+  a.sc_pe = m.sc_pe;
+  a.sc_imp = m.sc_imp;
+  a.sc_htop = m.sc_htop;
 }
 
 hipError_t launch(const StepArgs& a, const Workspace& w, hipStream_t s) {

@@ -56,6 +56,9 @@ struct SelectIO {
   float* mem_i;
   int32_t* mem_n;          // [b][H][n_prep]
   uint32_t* htop_mask;     // nullable [b]
+  float* out_p;            // nullable copies of this layer's scores before pooling: P
+  float* out_pe;           // [b][H][Tc], P over O' (H_top heads) [b][H][Tc],
+  float* out_imp;          // and I [b][Tc]
   uint32_t* spill_keys;    // [b][H][Tc] member arrays when members exceed the LDS capacity
   int32_t* spill_t;
   float* spill_ps;
@@ -146,6 +149,11 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
     if (t < a1) {
       sp[t - a0] = vp[k];
       se[t - a0] = ve[k];
+      // the caller's copy of the scores this work-group owns (no halo)
+      if (t >= t0 && t < t1) {
+        if (want_p && io.out_p) io.out_p[row + t] = vp[k];
+        if (want_e && io.out_pe) io.out_pe[row + t] = ve[k];
+      }
     }
   }
   if (want_p && h == 0 && io.psum_all) {
@@ -163,7 +171,10 @@ __device__ __forceinline__ void task_pool(const Problem& P, const SelectIO& io, 
 #pragma unroll
     for (int k = 0; k < kOwn; ++k) {
       const int t = t0 + (int)threadIdx.x + k * kThreads;
-      if (t < t1) io.imp[(int64_t)b * P.Tc + t] = si[k] * P.inv_go;
+      if (t < t1) {
+        io.imp[(int64_t)b * P.Tc + t] = si[k] * P.inv_go;
+        if (io.out_imp) io.out_imp[(int64_t)b * P.Tc + t] = si[k] * P.inv_go;
+      }
     }
   }
   __syncthreads();

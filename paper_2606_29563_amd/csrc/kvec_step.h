@@ -50,6 +50,10 @@ struct StepArgs {
   const float* p_ext;
   const float* imp_in;
   uint32_t* htop;
+  float* sc_p;               // nullable pipeline score outputs (see ModelIO)
+  float* sc_pe;
+  float* sc_imp;
+  uint32_t* sc_htop;
   int standalone_counts;     // selection reads complete n_t from the counts buffer
   Seg seg[ST_N];
 };
@@ -91,7 +95,11 @@ __device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int 
   io.mem_ps = reinterpret_cast<float*>(sb + a.w.mem_ps);
   io.mem_i = reinterpret_cast<float*>(sb + a.w.mem_i);
   io.mem_n = reinterpret_cast<int32_t*>(sb + a.w.mem_n);
-  io.htop_mask = a.htop;
+  io.htop_mask = a.sc_htop ? a.sc_htop + (int64_t)layer * a.P.batch : a.htop;
+  const int64_t per_p = (int64_t)a.P.batch * a.P.H * a.P.Tc;
+  io.out_p = a.sc_p ? a.sc_p + (int64_t)layer * per_p : nullptr;
+  io.out_pe = a.sc_pe ? a.sc_pe + (int64_t)layer * per_p : nullptr;
+  io.out_imp = a.sc_imp ? a.sc_imp + (int64_t)layer * a.P.batch * a.P.Tc : nullptr;
   io.spill_keys = reinterpret_cast<uint32_t*>(a.ws + a.w.spill);
   io.spill_t = reinterpret_cast<int32_t*>(a.ws + a.w.spill + a.w.spill_stride);
   io.spill_ps = reinterpret_cast<float*>(a.ws + a.w.spill + 2 * a.w.spill_stride);

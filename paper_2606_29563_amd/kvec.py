@@ -87,7 +87,7 @@ _lib = None
 
 EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_score_lse", "kvec_select_cover",
            "kvec_compact", "kvec_evict_layer", "kvec_evict_model", "kvec_evict_model_lse",
-           "kvec_evict_layer_lse",
+           "kvec_evict_layer_lse", "kvec_evict_model_scores",
            "kvec_profile_points", "kvec_profile_points_lse", "kvec_coverage",
            "kvec_decode_workspace_size", "kvec_decode_attention", "kvec_status_string"]
 
@@ -116,6 +116,8 @@ def load() -> ctypes.CDLL:
                                          vp, vp, vp, sz, vp]
     lib.kvec_evict_model_lse.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp,
                                          vp, sz, vp, ctypes.POINTER(vp)]
+    lib.kvec_evict_model_scores.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp,
+                                            vp, vp, vp, vp, sz, vp]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
     lib.kvec_decode_workspace_size.argtypes = [P, i32, ctypes.POINTER(sz)]
     lib.kvec_decode_attention.argtypes = [P, vp, I64x, vp, vp, I64x, i32, vp, vp, vp, sz, vp]
@@ -229,6 +231,21 @@ def kvec_evict_model(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, ws
                                    _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream), ev),
            "kvec_evict_model")
+
+
+def kvec_evict_model_scores(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, p_raw_out,
+                            p_ext_out, imp_out, htop_out, ws, stream=None) -> None:
+    """As kvec_evict_model, also writing each layer's scores before pooling:
+    p_raw_out, p_ext_out fp32 [L][b][H][Tc] (P over O' for the H_top heads only),
+    imp_out fp32 [L][b][Tc], htop_out int32/uint32 [L][b] (H_top bit masks)."""
+    c = cfg.c()
+    _check(load().kvec_evict_model_scores(ctypes.byref(c), _ptr(q_win), _strides(q_win, 4),
+                                          _ptr(k), _strides(k, 4), _ptr(v), _strides(v, 4),
+                                          _ptr(cover_bits), _ptr(idx), _ptr(k_out), _ptr(v_out),
+                                          _ptr(p_raw_out), _ptr(p_ext_out), _ptr(imp_out),
+                                          _ptr(htop_out), _ptr(ws),
+                                          ws.numel() * ws.element_size(), _stream(stream)),
+           "kvec_evict_model_scores")
 
 
 def kvec_evict_layer_lse(cfg: Config, layer: int, q_win, lse, k, v, cover_bits, idx, k_out, v_out,

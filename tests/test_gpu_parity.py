@@ -190,15 +190,24 @@ def oracle_lse_tensor(w):
     return torch.from_numpy(out).cuda()
 
 
-def _e2e(kv, w, check_layers=None, lse=False):
-    """Run the whole-model driver (kvec_evict_model, or kvec_evict_model_lse on
-    the oracle's row normalisers) and check sampled layers teacher-forced."""
+def _e2e(kv, w, check_layers=None, lse=False, scores=None, same_as_model=False):
+    """Run the whole-model driver and check layers teacher-forced (the oracle's
+    layer l uses the device's bitmap rows of layers < l).
+
+    The driver is kvec_evict_model_lse on the oracle's row normalisers when
+    lse=True; else kvec_evict_model_scores (scores=True, the default), whose
+    per-layer P, P over O' of the H_top heads and I are then compared element
+    by element with the oracle at SCORE_RTOL, or kvec_evict_model.  With
+    same_as_model=True kvec_evict_model also runs and must give bit-identical
+    indices, bitmaps and caches (the scores variant runs the same pipeline)."""
     import torch
+    scores = (not lse) if scores is None else scores
     cfg = kv.Config.from_workload(w)
     ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
     _say(f"[e2e] {w.name}{' (given lse)' if lse else ''}: generating inputs")
     q, k, v = model_tensors(w)
     L, H, B, T, d = w.n_layers, w.n_kv_heads, w.budget, w.seq_len, w.head_dim
+    Tc = w.candidates
     W = (T + 63) // 64
     bits = torch.empty((w.batch, L, W), dtype=torch.int64, device="cuda")
     idx = torch.empty((L, w.batch, H, B), dtype=torch.int32, device="cuda")
@@ -206,22 +215,54 @@ def _e2e(kv, w, check_layers=None, lse=False):
     vo = torch.empty_like(ko)
     if lse:
         kv.kvec_evict_model_lse(cfg, q, oracle_lse_tensor(w), k, v, bits, idx, ko, vo, ws)
+    elif scores:
+        sp = torch.full((L, w.batch, H, Tc), float("nan"), dtype=torch.float32, device="cuda")
+        spe = torch.full_like(sp, float("nan"))
+        simp = torch.full((L, w.batch, Tc), float("nan"), dtype=torch.float32, device="cuda")
+        shtop = torch.zeros((L, w.batch), dtype=torch.int32, device="cuda")
+        kv.kvec_evict_model_scores(cfg, q, k, v, bits, idx, ko, vo, sp, spe, simp, shtop, ws)
     else:
         kv.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws)
     torch.cuda.synchronize()
     _say(f"[e2e] {w.name}: device step done")
+    if same_as_model:
+        bits2, idx2 = torch.empty_like(bits), torch.empty_like(idx)
+        ko2, vo2 = torch.empty_like(ko), torch.empty_like(vo)
+        kv.kvec_evict_model(cfg, q, k, v, bits2, idx2, ko2, vo2, ws)
+        torch.cuda.synchronize()
+        raw = torch.int16 if k.dtype == torch.bfloat16 else torch.int32
+        assert torch.equal(idx, idx2) and torch.equal(bits, bits2)
+        assert torch.equal(ko.view(raw), ko2.view(raw)) and torch.equal(vo.view(raw), vo2.view(raw))
+        _say("   kvec_evict_model gives the same indices, bitmaps and caches")
     gi = idx.cpu().numpy()
     gb = bits.cpu().numpy().view(np.uint64)
+    if scores and not lse:
+        gp, gpe, gimp, ght = (sp.cpu().numpy(), spe.cpu().numpy(), simp.cpu().numpy(),
+                              shtop.cpu().numpy())
+    ibits = torch.int16 if k.dtype == torch.bfloat16 else torch.int32
     M = B - w.window
     kp = orc.preserve_count(B, w.window, w.beta)
     layers = range(L) if check_layers is None else check_layers
     tot_m = tot = 0
+    worst = 0.0
+    cache = {}
     for l in layers:
         for b in range(w.batch):
             p, pe, imp = oracle_scores(w, l, b)
+            if b == 0:
+                cache[l] = (p, pe, imp)
             n_t = counts_before(gb[b], l, T)
             res = orc.evict_layer_from_scores(orc.to_f32(p), orc.to_f32(pe), orc.to_f32(imp),
                                               n_t, l, w)
+            if scores and not lse:
+                # the pipeline's own scores, element by element
+                hs = [h for h in range(H) if (int(ght[l, b]) >> h) & 1]
+                assert sorted(hs) == sorted(int(x) for x in res.htop), (l, b, hs, res.htop)
+                e = [rel_err(gp[l, b], p), rel_err(gimp[l, b], imp)]
+                if hs:
+                    e.append(rel_err(gpe[l, b, hs], pe[hs]))
+                worst = max(worst, max(e))
+                assert max(e) <= SCORE_RTOL, (l, b, e)
             m, t, bad = agreement(gi[l, b], res, M, kp)
             tot_m += m
             tot += t
@@ -231,12 +272,27 @@ def _e2e(kv, w, check_layers=None, lse=False):
             assert np.all(np.diff(gi[l, b, :, :M], axis=1) > 0)
             np.testing.assert_array_equal(bits_to_bool(gb[b, l], T),
                                           orc.layer_bits(gi[l, b], T))
-            # gather is byte-exact for the GPU's own indices
-            kk = k[l, b].cpu().view(torch.int16).numpy()
-            np.testing.assert_array_equal(ko[l, b].cpu().view(torch.int16).numpy(),
-                                          orc.gather_rows(kk, gi[l, b]))
-        _say(f"   layer {l}: agreement so far {tot_m / tot:.5f}")
+            # gather of K and V is byte-exact for the GPU's own indices
+            for src, out in ((k, ko), (v, vo)):
+                xx = src[l, b].cpu().view(ibits).numpy()
+                np.testing.assert_array_equal(out[l, b].cpu().view(ibits).numpy(),
+                                              orc.gather_rows(xx, gi[l, b]))
+        _say(f"   layer {l}: agreement so far {tot_m / tot:.5f}"
+             + (f", worst score rel err {worst:.2e}" if scores and not lse else ""))
     assert tot_m / tot >= AGREE_MIN
+    if check_layers is None and w.batch == 1:
+        # free-running agreement (the oracle on its own bitmaps): reported only
+        own, fm, ft = [], 0, 0
+        for l in range(L):
+            p, pe, imp = cache[l]
+            n_t = orc.counts_from_bits(own) if own else np.zeros(T, np.int64)
+            res = orc.evict_layer_from_scores(orc.to_f32(p), orc.to_f32(pe), orc.to_f32(imp),
+                                              n_t, l, w)
+            own.append(res.bits)
+            for h in range(H):
+                fm += len(set(gi[l, 0, h, :M].tolist()) & set(res.idx[h, :M].tolist()))
+                ft += M
+        _say(f"   free-running agreement (not gated): {fm / ft:.5f}")
     # coverage equals the union of the kept index sets
     cnt = torch.empty((w.batch,), dtype=torch.int64, device="cuda")
     kv.kvec_coverage(cfg, bits, L - 1, cnt)
@@ -314,16 +370,18 @@ def test_full_llama8b_4k_every_layer(gpu_lib):
     _e2e(gpu_lib, synth.workload(1))
 
 
-def test_full_llama8b_32k_sampled_layers(gpu_lib):
-    _e2e(gpu_lib, synth.workload(2), check_layers=[0, 1, 15, 31])
+def test_full_llama8b_32k_every_layer(gpu_lib):
+    """The benchmarked workload: every layer's scores, indices, bitmaps and
+    gathered K/V; kvec_evict_model must match the scores variant exactly."""
+    _e2e(gpu_lib, synth.workload(2), same_as_model=True)
 
 
-def test_full_llama8b_16k_batch8_sampled_layers(gpu_lib):
-    _e2e(gpu_lib, synth.workload(3), check_layers=[0, 31])
+def test_full_llama8b_16k_batch8_layers(gpu_lib):
+    _e2e(gpu_lib, synth.workload(3), check_layers=[0, 1, 2, 3, 15, 16, 30, 31])
 
 
-def test_full_llama8b_128k_sampled_layers(gpu_lib):
-    _e2e(gpu_lib, synth.workload(4), check_layers=[0, 31])
+def test_full_llama8b_128k_layers(gpu_lib):
+    _e2e(gpu_lib, synth.workload(4), check_layers=list(range(0, 32, 4)) + [31])
 
 
 def test_full_qwen7b_32k_sampled_layers(gpu_lib):
@@ -331,7 +389,7 @@ def test_full_qwen7b_32k_sampled_layers(gpu_lib):
     _e2e(gpu_lib, synth.workload(5), check_layers=[0, 1, 27])
 
 
-@pytest.mark.parametrize("wi", [2, 3, 4, 5], ids=["32k", "16k-b8", "128k", "qwen7b-32k"])
+@pytest.mark.parametrize("wi", [1, 2, 3, 4, 5], ids=["4k", "32k", "16k-b8", "128k", "qwen7b-32k"])
 def test_full_size_scores(gpu_lib, wi):
     """kvec_score on one layer of a full-size shape against the oracle scores."""
     import torch
@@ -355,3 +413,122 @@ def test_full_size_scores(gpu_lib, wi):
          rel_err(imp[0].cpu().numpy(), rimp))
     _say(f"[score] {w.name} layer {layer}: rel err P {e[0]:.2e} P' {e[1]:.2e} I {e[2]:.2e}")
     assert max(e) <= SCORE_RTOL, e
+
+
+# ---------------------------------------------------------------------------
+# Exact ties at scale and the exact row-normaliser fallback
+# ---------------------------------------------------------------------------
+
+def test_all_ties_member_spill(gpu_lib):
+    """Zero queries: every logit is 0, so P[t] = (H_T - H_{T-O}) / O for every
+    candidate t (the closed form the oracle pins) and every head, I equals P,
+    and every ranking is decided by the tie rule alone (score descending, index
+    ascending; lower head first for sigma).  With 12000 candidates all in one
+    histogram bin the selection's member lists exceed what LDS holds and take
+    the spill path.  Indices and bitmaps are compared bit-exactly with the
+    oracle run free on its own bitmaps."""
+    import torch
+    kv = gpu_lib
+    w = _small("all-ties", 12032, 32, 64, 2, 2, 64, "bf16", B=256, layers=3, delta=1)
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    L, H, B, T, d, Tc = w.n_layers, w.n_kv_heads, w.budget, w.seq_len, w.head_dim, w.candidates
+    _, k, v = model_tensors(w)
+    q = torch.zeros((L, 1, w.n_q_heads, w.rows, d), dtype=k.dtype, device="cuda")
+    W = (T + 63) // 64
+    bits = torch.empty((1, L, W), dtype=torch.int64, device="cuda")
+    idx = torch.empty((L, 1, H, B), dtype=torch.int32, device="cuda")
+    ko = torch.empty((L, 1, H, B, d), dtype=k.dtype, device="cuda")
+    vo = torch.empty_like(ko)
+    sp = torch.empty((L, 1, H, Tc), dtype=torch.float32, device="cuda")
+    spe = torch.empty_like(sp)
+    simp = torch.empty((L, 1, Tc), dtype=torch.float32, device="cuda")
+    sht = torch.empty((L, 1), dtype=torch.int32, device="cuda")
+    kv.kvec_evict_model_scores(cfg, q, k, v, bits, idx, ko, vo, sp, spe, simp, sht, ws)
+    torch.cuda.synchronize()
+    gi, gp = idx.cpu().numpy(), sp.cpu().numpy()
+    gb = bits.cpu().numpy().view(np.uint64)
+    qz = np.zeros((w.n_q_heads, w.rows, d))
+    own = []
+    for l in range(L):
+        # the device's scores are one value for every candidate of every head
+        assert np.all(gp[l] == gp[l, 0, 0, 0]), l
+        kf = synth.to_f64(synth.keys(w, l, 0), w.dtype)
+        p, pe, imp = orc.score_layer(qz, kf, w.window)
+        assert rel_err(gp[l, 0], p) <= SCORE_RTOL
+        n_t = orc.counts_from_bits(own) if own else np.zeros(T, np.int64)
+        res = orc.evict_layer_from_scores(p, pe, imp, n_t, l, w)
+        np.testing.assert_array_equal(gi[l, 0], res.idx, err_msg=f"layer {l}")
+        np.testing.assert_array_equal(bits_to_bool(gb[0, l], T), res.bits)
+        assert int(sht[l, 0]) == 1, int(sht[l, 0])          # sigma tie -> head 0
+        own.append(res.bits)
+        _say(f"   layer {l}: {Tc} tied candidates, indices bit-exact")
+
+
+def _fallback_inputs(w):
+    """Random bf16 window queries and keys with two planted pairs whose logit is
+    200 (about 288 in base 2): window row Wn-1 with key 200 (in the second key
+    tile of 128 but not among its first 16 keys, so that tile's running sum
+    overflows past its block reference) and window row Wn-2 with key 3 (among
+    the first 16 keys of the first tile, so that tile's block reference is huge
+    and the other rows' sums underflow)."""
+    g = np.random.default_rng(11)
+    d, T, Wn = w.head_dim, w.seq_len, w.rows
+    q = (0.5 * g.standard_normal((w.n_q_heads, Wn, d))).astype(np.float32)
+    k = g.standard_normal((w.n_kv_heads, T, d)).astype(np.float32)
+    q[:, Wn - 1] = 0.0
+    q[:, Wn - 1, 0] = 40.0
+    k[:, 200] = 0.0
+    k[:, 200, 0] = 40.0
+    q[:, Wn - 2] = 0.0
+    q[:, Wn - 2, 1] = 40.0
+    k[:, 3] = 0.0
+    k[:, 3, 1] = 40.0
+    # bf16 storage by truncation (any bf16 values serve; 40 and 0 are exact)
+    qb = (q.view(np.uint32) >> 16).astype(np.uint16)
+    kb = (k.view(np.uint32) >> 16).astype(np.uint16)
+    return qb, kb
+
+
+def test_score_exact_normaliser_fallback(gpu_lib):
+    """Key tiles whose partial sums leave the fp32 range of the fast path are
+    recomputed exactly by the row-normaliser stage; the scores still match the
+    oracle (both through kvec_score and through the pipeline)."""
+    import torch
+    kv = gpu_lib
+    w = _small("fallback", 600, 8, 16, 1, 1, 64, "bf16", B=64, layers=2, hh=0.0)
+    cfg = kv.Config.from_workload(w)
+    ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    qb, kb = _fallback_inputs(w)
+    ref = orc.window_scores(synth.to_f64(qb, "bf16"), synth.to_f64(kb, "bf16"), w.window)
+    q, k = to_device(qb, w)[None], to_device(kb, w)[None]
+    Tc = w.candidates
+    p = torch.empty((1, 1, Tc), dtype=torch.float32, device="cuda")
+    pe, imp = torch.empty_like(p), torch.empty((1, Tc), dtype=torch.float32, device="cuda")
+    kv.kvec_score(cfg, q, k, p, pe, imp, ws)
+    torch.cuda.synchronize()
+    e = (rel_err(p[0].cpu().numpy(), ref[0]), rel_err(pe[0].cpu().numpy(), ref[1]),
+         rel_err(imp[0].cpu().numpy(), ref[2]))
+    _say(f"   kvec_score: rel err P {e[0]:.2e} P' {e[1]:.2e} I {e[2]:.2e}")
+    assert max(e) <= SCORE_RTOL, e
+    # the two planted keys take nearly all of their rows' attention
+    assert p[0, 0, 200] > 0.1 and p[0, 0, 3] > 0.1
+    # the same inputs in both layers of the pipeline
+    L = w.n_layers
+    qq, kk = q[None].expand(L, -1, -1, -1, -1), k[None].expand(L, -1, -1, -1, -1)
+    vv = torch.zeros_like(kk)
+    bits = torch.empty((1, L, (w.seq_len + 63) // 64), dtype=torch.int64, device="cuda")
+    idx = torch.empty((L, 1, 1, w.budget), dtype=torch.int32, device="cuda")
+    ko = torch.empty((L, 1, 1, w.budget, w.head_dim), dtype=k.dtype, device="cuda")
+    vo = torch.empty_like(ko)
+    sp = torch.empty((L, 1, 1, Tc), dtype=torch.float32, device="cuda")
+    spe = torch.empty_like(sp)
+    simp = torch.empty((L, 1, Tc), dtype=torch.float32, device="cuda")
+    sht = torch.empty((L, 1), dtype=torch.int32, device="cuda")
+    kv.kvec_evict_model_scores(cfg, qq, kk, vv, bits, idx, ko, vo, sp, spe, simp, sht, ws)
+    torch.cuda.synchronize()
+    for l in range(L):
+        e = [rel_err(sp[l, 0].cpu().numpy(), ref[0]), rel_err(simp[l, 0].cpu().numpy(), ref[2])]
+        if int(sht[l, 0]) & 1:
+            e.append(rel_err(spe[l, 0].cpu().numpy(), ref[1]))
+        assert max(e) <= SCORE_RTOL, (l, e)
