@@ -300,6 +300,23 @@ kvec_status kvec_decode_attention(const kvec_config* cfg,
                                   const int32_t* idx, float* out,
                                   void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* kvec_decode_attention for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation, with no workspace argument.  The
+ * partial states live in a fixed device array of the library (4 MiB per
+ * device, held until the process ends); the call allocates nothing.
+ *   Arguments, outputs and errors as kvec_decode_attention, plus
+ *   KVEC_ERR_WORKSPACE when the partial states would exceed 4 MiB, i.e. when
+ *   kvec_decode_workspace_size(cfg, n_ctx) > 4 MiB (checked before any
+ *   device call).  Every call on one device shares the array: calls that
+ *   overlap on the same device (other streams, other host threads) race.
+ *   The device is the current one; `stream` must belong to it. */
+kvec_status kvec_decode_attention_noalloc(const kvec_config* cfg,
+                                          const void* q, const int64_t q_strides[2],
+                                          const void* k_cache, const void* v_cache,
+                                          const int64_t cache_strides[2], int32_t n_ctx,
+                                          const int32_t* idx, float* out, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* kvec_status_string(kvec_status status);
 

@@ -495,24 +495,62 @@ kvec_status kvec_decode_workspace_size(const kvec_config* cfg, int32_t n_ctx, si
   return KVEC_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Validation shared by both decode entry points; fills the plan.
+kvec_status decode_check(const kvec_config* cfg, Geometry* g, const void* q,
+                         const int64_t q_strides[2], const void* k_cache, const void* v_cache,
+                         const int64_t cache_strides[2], int32_t n_ctx, const int32_t* idx,
+                         const float* out, DecodePlan* pl) {
+  const kvec_status st = make_geometry(cfg, g);
+  if (st != KVEC_OK) return st;
+  if (n_ctx < 1 || n_ctx > (1 << 20) || (idx && n_ctx < g->p.B)) return KVEC_ERR_INVALID;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !out ||
+      ((uintptr_t)out & 3u) != 0 || !strides_ok(q_strides, 2, g->p.esize) ||
+      !strides_ok(cache_strides, 2, g->p.esize))
+    return KVEC_ERR_INVALID;
+  *pl = decode_plan(g->p, n_ctx);
+  return KVEC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 kvec_status kvec_decode_attention(const kvec_config* cfg, const void* q, const int64_t q_strides[2],
                                   const void* k_cache, const void* v_cache,
                                   const int64_t cache_strides[2], int32_t n_ctx,
                                   const int32_t* idx, float* out, void* ws, size_t ws_bytes,
                                   hipStream_t stream) {
   Geometry g;
-  const kvec_status st = make_geometry(cfg, &g);
+  DecodePlan pl;
+  const kvec_status st =
+      decode_check(cfg, &g, q, q_strides, k_cache, v_cache, cache_strides, n_ctx, idx, out, &pl);
   if (st != KVEC_OK) return st;
-  if (n_ctx < 1 || n_ctx > (1 << 20) || (idx && n_ctx < g.p.B)) return KVEC_ERR_INVALID;
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !out ||
-      ((uintptr_t)out & 3u) != 0 || !strides_ok(q_strides, 2, g.p.esize) ||
-      !strides_ok(cache_strides, 2, g.p.esize))
-    return KVEC_ERR_INVALID;
-  const DecodePlan pl = decode_plan(g.p, n_ctx);
   if (ws_bytes < pl.ws_bytes) return KVEC_ERR_WORKSPACE;
   if (!aligned16(ws)) return KVEC_ERR_INVALID;
   return dev(run_decode(g, q, q_strides, k_cache, v_cache, cache_strides, n_ctx, idx, out, ws,
                         stream));
+}
+
+kvec_status kvec_decode_attention_noalloc(const kvec_config* cfg, const void* q,
+                                          const int64_t q_strides[2], const void* k_cache,
+                                          const void* v_cache, const int64_t cache_strides[2],
+                                          int32_t n_ctx, const int32_t* idx, float* out,
+                                          hipStream_t stream) {
+  Geometry g;
+  DecodePlan pl;
+  const kvec_status st =
+      decode_check(cfg, &g, q, q_strides, k_cache, v_cache, cache_strides, n_ctx, idx, out, &pl);
+  if (st != KVEC_OK) return st;
+  // the partial states must fit the fixed scratch (checked before any device call)
+  if (pl.ws_bytes > kDecodeScratchBytes) return KVEC_ERR_WORKSPACE;
+  void* scratch = nullptr;
+  if (decode_scratch(&scratch) != hipSuccess) return KVEC_ERR_DEVICE;
+  return dev(run_decode(g, q, q_strides, k_cache, v_cache, cache_strides, n_ctx, idx, out,
+                        scratch, stream));
 }
 
 int32_t kvec_profile_points_lse(const kvec_config* cfg) {

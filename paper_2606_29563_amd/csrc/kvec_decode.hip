@@ -19,6 +19,8 @@
 //   combine  one work-group per (query head, sequence) merges the chunks.
 #include <math.h>
 
+#include <mutex>
+
 #include "kvec_internal.h"
 #include "kvec_score_dev.h"  // DPP lane moves
 
@@ -277,6 +279,38 @@ DecFn dec_pick(int G) {
 }
 
 }  // namespace
+
+// Partial states of the allocation-free entry point: a file-scope device
+// array instead of a caller workspace.  Each device the library runs on holds
+// its own copy until the process ends; its device address is taken once per
+// device (with that device current) and kept, and only that address is
+// passed to the kernels.  Every call on a device shares the array, so calls
+// that overlap on one device race.  Nothing in it needs clearing: the
+// partial kernel writes every chunk state the combine kernel reads.
+static __device__ __align__(256) char scratch[kDecodeScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of `scratch`, per device
+}  // namespace
+
+hipError_t decode_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch[dev] = p;
+  }
+  *ptr = g_scratch[dev];
+  return hipSuccess;
+}
 
 // Row chunk per work-group: enough work-groups to cover the chip (about
 // 512 over batch x heads), at least 64 rows each.

@@ -141,6 +141,10 @@ struct DecodePlan {
   size_t ws_bytes;  // partial states [b][HQ][S][d + 2] floats
 };
 DecodePlan decode_plan(const Problem& P, int n_ctx);
+// Fixed device scratch of kvec_decode_attention_noalloc (partial states).
+constexpr size_t kDecodeScratchBytes = (size_t)4 << 20;
+// Device address of that scratch on the current device (set up on first use).
+hipError_t decode_scratch(void** ptr);
 hipError_t run_decode(const Geometry& g, const void* q, const int64_t qs[2], const void* k,
                       const void* v, const int64_t cs[2], int n_ctx, const int32_t* idx, float* out,
                       void* ws, hipStream_t s);

@@ -89,7 +89,8 @@ EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_score_lse", "kvec_select_c
            "kvec_compact", "kvec_evict_layer", "kvec_evict_model", "kvec_evict_model_lse",
            "kvec_evict_layer_lse", "kvec_evict_model_scores",
            "kvec_profile_points", "kvec_profile_points_lse", "kvec_coverage",
-           "kvec_decode_workspace_size", "kvec_decode_attention", "kvec_status_string"]
+           "kvec_decode_workspace_size", "kvec_decode_attention", "kvec_decode_attention_noalloc",
+           "kvec_status_string"]
 
 
 def load() -> ctypes.CDLL:
@@ -118,6 +119,7 @@ def load() -> ctypes.CDLL:
                                          vp, sz, vp, ctypes.POINTER(vp)]
     lib.kvec_evict_model_scores.argtypes = [P, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp,
                                             vp, vp, vp, vp, sz, vp]
+    lib.kvec_decode_attention_noalloc.argtypes = [P, vp, I64x, vp, vp, I64x, i32, vp, vp, vp]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
     lib.kvec_decode_workspace_size.argtypes = [P, i32, ctypes.POINTER(sz)]
     lib.kvec_decode_attention.argtypes = [P, vp, I64x, vp, vp, I64x, i32, vp, vp, vp, sz, vp]
@@ -312,3 +314,18 @@ def kvec_decode_attention(cfg: Config, q, k_cache, v_cache, out, ws, idx=None, n
                                         _ptr(v_cache), _strides(k_cache, 2), n, _ptr(idx),
                                         _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
                                         _stream(stream)), "kvec_decode_attention")
+
+
+def kvec_decode_attention_noalloc(cfg: Config, q, k_cache, v_cache, out, idx=None, n_ctx=None,
+                                  stream=None) -> None:
+    """kvec_decode_attention without a workspace: the partial states use the
+    library's fixed 4 MiB device scratch (calls overlapping on one device race)."""
+    c = cfg.c()
+    n = k_cache.shape[2] if n_ctx is None else n_ctx
+    assert k_cache.stride()[:2] == v_cache.stride()[:2], "K and V caches share their strides"
+    assert k_cache.stride(2) == k_cache.shape[3] and v_cache.stride(2) == v_cache.shape[3], \
+        "cache rows must be contiguous"
+    _check(load().kvec_decode_attention_noalloc(ctypes.byref(c), _ptr(q), _strides(q, 2),
+                                                _ptr(k_cache), _ptr(v_cache), _strides(k_cache, 2),
+                                                n, _ptr(idx), _ptr(out), _stream(stream)),
+           "kvec_decode_attention_noalloc")

@@ -160,6 +160,26 @@ def test_decode_validation():
     assert call(ws_bytes=16) == kvec.KVEC_ERR_WORKSPACE
 
 
+def test_noalloc_decode_validation():
+    """The allocation-free decode entry rejects, before any device call, what
+    kvec_decode_attention rejects and plans beyond its fixed 4 MiB scratch."""
+    lib = kvec.load()
+    fake = ctypes.c_void_p(1 << 20)
+    qs = (ctypes.c_int64 * 2)(32 * 128, 128)
+    cs = (ctypes.c_int64 * 2)(8 * 1024 * 128, 1024 * 128)
+    def call(cfg, q=fake, n=1024, idx=None, out=fake):
+        c = cfg.c()
+        return lib.kvec_decode_attention_noalloc(ctypes.byref(c), q, qs, fake, fake, cs, n, idx,
+                                                 out, None)
+    assert call(_cfg(), n=0) == kvec.KVEC_ERR_INVALID
+    assert call(_cfg(), n=1000, idx=fake) == kvec.KVEC_ERR_INVALID
+    assert call(_cfg(), out=None) == kvec.KVEC_ERR_INVALID
+    assert call(_cfg(batch=0)) == kvec.KVEC_ERR_INVALID
+    big = _cfg(batch=256)   # 256 x 8 heads: one chunk each, 4.26 MB of partial states
+    assert kvec.kvec_decode_workspace_size(big, 1024) > 4 << 20
+    assert call(big) == kvec.KVEC_ERR_WORKSPACE
+
+
 def test_profile_points():
     assert kvec.kvec_profile_points(_cfg()) == 32 + 12
     assert kvec.kvec_profile_points_lse(_cfg()) == 32 + 8
