@@ -17,6 +17,10 @@
 //            of a wave by shuffles, across waves through LDS, and the
 //            chunk's (max, sum, V[d]) go to the workspace.
 //   combine  one work-group per (query head, sequence) merges the chunks.
+// (A single launch in which the last partial work-group of each head
+// combines, behind an arrival counter, measured slower: the combine then
+// runs as a serial tail after the slowest chunk, and the release/acquire
+// fences it needs across the XCDs' caches cost more than the launch saved.)
 #include <math.h>
 
 #include <mutex>
@@ -222,15 +226,39 @@ __global__ __launch_bounds__(kDecThreads) void decode_partial(DecArgs a) {
 }
 
 // Chunk states are read in batches of kDecBatch with every load of a batch in
-// flight at once (the chunks were written by other XCDs, so each read is a
-// memory round trip): first the maximum, then the rescaled sums.
+// flight at once (the chunks were written by other work-groups, on other
+// XCDs, so each read is a memory round trip): up to kDecBatch chunks in one
+// round trip, more in two passes (the maximum, then the rescaled sums).  Both
+// orders add the chunks in ascending order.
 constexpr int kDecBatch = 16;
 
 template <int D>
-__global__ __launch_bounds__(D) void decode_combine(DecArgs a) {
-  const int j = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
+__device__ __forceinline__ float combine_elem(const DecArgs& a, int b, int j, int e) {
   const float* pp = a.part + ((int64_t)b * a.HQ + j) * a.S * (D + 2);
-  float m = -INFINITY;
+  float m = -INFINITY, l = 0.f, av = 0.f;
+  if (a.S <= kDecBatch) {
+    float ms[kDecBatch], ls[kDecBatch], as[kDecBatch];
+#pragma unroll
+    for (int i = 0; i < kDecBatch; ++i) {
+      const bool ok = i < a.S;
+      const float* q = pp + (int64_t)(ok ? i : 0) * (D + 2);
+      ms[i] = ok ? q[0] : -INFINITY;
+      ls[i] = q[1];
+      as[i] = q[2 + e];
+    }
+#pragma unroll
+    for (int i = 0; i < kDecBatch; ++i) m = fmaxf(m, ms[i]);
+    if (m != -INFINITY) {
+#pragma unroll
+      for (int i = 0; i < kDecBatch; ++i) {
+        // empty chunks (m = -inf) weigh exp2(-inf) = 0
+        const float f = __builtin_amdgcn_exp2f(ms[i] - m);
+        l = fmaf(ls[i], f, l);
+        av = fmaf(as[i], f, av);
+      }
+    }
+    return l > 0.f ? av / l : 0.f;
+  }
   for (int s0 = 0; s0 < a.S; s0 += kDecBatch) {
     float ms[kDecBatch];
 #pragma unroll
@@ -238,7 +266,6 @@ __global__ __launch_bounds__(D) void decode_combine(DecArgs a) {
 #pragma unroll
     for (int i = 0; i < kDecBatch; ++i) m = fmaxf(m, ms[i]);
   }
-  float l = 0.f, av = 0.f;
   if (m != -INFINITY) {
     for (int s0 = 0; s0 < a.S; s0 += kDecBatch) {
       float ms[kDecBatch], ls[kDecBatch], as[kDecBatch];
@@ -252,14 +279,19 @@ __global__ __launch_bounds__(D) void decode_combine(DecArgs a) {
       }
 #pragma unroll
       for (int i = 0; i < kDecBatch; ++i) {
-        // empty chunks (m = -inf) weigh exp2(-inf) = 0
         const float f = __builtin_amdgcn_exp2f(ms[i] - m);
         l = fmaf(ls[i], f, l);
         av = fmaf(as[i], f, av);
       }
     }
   }
-  a.out[((int64_t)b * a.HQ + j) * D + e] = l > 0.f ? av / l : 0.f;
+  return l > 0.f ? av / l : 0.f;
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void decode_combine(DecArgs a) {
+  const int j = blockIdx.x, b = blockIdx.y, e = threadIdx.x;
+  a.out[((int64_t)b * a.HQ + j) * D + e] = combine_elem<D>(a, b, j, e);
 }
 
 typedef void (*DecFn)(DecArgs);

@@ -313,7 +313,11 @@ struct ScoreTile {
 
   using KR = KeyRing<TT, D>;
   Frag<TT, D> qf[NB];
-  Frag<TT, D> kf[2];              // key fragments of the current and next step
+  // key fragments of the current and the next step; with seven or eight row
+  // blocks one register set (the next step's read waits for this step's
+  // products to be issued), which keeps the queries and sums in registers
+  static constexpr int NKF = NB >= 7 ? 1 : 2;
+  Frag<TT, D> kf[NKF];
   uint4* ring;                    // this wave's LDS slots
   __amdgpu_buffer_rsrc_t krsrc;   // keys [0, tend) of (b, h)
   int kstride;                    // bytes between consecutive keys
@@ -462,7 +466,7 @@ struct ScoreTile {
 
   template <int F>
   __device__ __forceinline__ void read_frag(int u) {
-    kf[F].load_lds(ring + u * (KR::SLOT / 16), n, c, KR::SWZ);
+    kf[F % NKF].load_lds(ring + u * (KR::SLOT / 16), n, c, KR::SWZ);
   }
 
   template <int F>
@@ -474,7 +478,7 @@ struct ScoreTile {
 #pragma unroll
     for (int j = 0; j < Frag<TT, D>::KS; ++j)
 #pragma unroll
-      for (int bk = 0; bk < NB; ++bk) acc[bk] = mma1<D>(qf[bk], kf[F], acc[bk], j);
+      for (int bk = 0; bk < NB; ++bk) acc[bk] = mma1<D>(qf[bk], kf[F % NKF], acc[bk], j);
   }
 
   // Pass-2 epilogue shapes, fixed per wave before the key loop.  EP_GEN
@@ -635,6 +639,13 @@ struct ScoreTile {
     if constexpr (PASS == 2) {
       if (exch && (((s + 1) * 16) & (P.SK - 1)) == 0) exchange(s);
     }
+    if constexpr (NB >= 7) {
+      // The next step's products read this fragment only after this step's
+      // exponentials: with seven or eight blocks two sets of products would
+      // not fit in registers next to the queries.
+#pragma unroll
+      for (int j = 0; j < Frag<TT, D>::KS; ++j) asm volatile("" : "+v"(kf[(F ^ 1) % NKF].v[j]));
+    }
     // Keep the steps in program order (the next step's waits stay after
     // this step's work).
     __builtin_amdgcn_sched_barrier(0);
@@ -784,31 +795,31 @@ __device__ __forceinline__ void score_tile(const Problem& P, const ScoreIO& io, 
 // recurrence m' = max(m, x), l' = l * 2^(m - m') + 2^(x - m'), dot products
 // on the vector ALU.  Only used when the tile's fast partial overflowed.
 template <class TT, int D>
-__device__ __noinline__ float2 lse_partial_exact(const Problem P, const char* q, const char* k,
+__device__ __forceinline__ float2 lse_partial_exact(const Problem P, const char* q, const char* k,
                                                   int64_t qrow, int64_t kb, int64_t ks_t, int pos,
                                                   int kt) {
   constexpr int ES = elem_bytes<TT>();
-  float qv[D];
-  for (int i = 0; i < D; ++i) {
-    if constexpr (ES == 2) {
-      const uint16_t u = reinterpret_cast<const uint16_t*>(q + qrow * ES)[i];
-      qv[i] = __uint_as_float((uint32_t)u << 16);
-    } else {
-      qv[i] = reinterpret_cast<const float*>(q + qrow * ES)[i];
-    }
-  }
+  constexpr int EPP = 16 / ES;  // elements per 16-byte piece
+  // 16-byte pieces of the query row and each key row, converted as they are
+  // read (no private copy of the row)
+  const uint4* qp = reinterpret_cast<const uint4*>(q + qrow * ES);
   float m = -INFINITY, l = 0.f;
   const int t1 = min((kt + 1) * P.tile1, min(P.T, pos + 1));
   for (int t = kt * P.tile1; t < t1; ++t) {
-    const char* kr = k + (kb + (int64_t)t * ks_t) * ES;
+    const uint4* kp = reinterpret_cast<const uint4*>(k + (kb + (int64_t)t * ks_t) * ES);
     float dot = 0.f;
-    for (int i = 0; i < D; ++i) {
-      float kv;
-      if constexpr (ES == 2)
-        kv = __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(kr)[i] << 16);
-      else
-        kv = reinterpret_cast<const float*>(kr)[i];
-      dot = fmaf(qv[i], kv, dot);
+    for (int pc = 0; pc < D / EPP; ++pc) {
+      const uint4 a = qp[pc], bv = kp[pc];
+      const uint32_t qa[4] = {a.x, a.y, a.z, a.w}, ka[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        if constexpr (ES == 2) {
+          dot = fmaf(__uint_as_float(qa[w] << 16), __uint_as_float(ka[w] << 16), dot);
+          dot = fmaf(__uint_as_float(qa[w] & 0xffff0000u), __uint_as_float(ka[w] & 0xffff0000u), dot);
+        } else {
+          dot = fmaf(__uint_as_float(qa[w]), __uint_as_float(ka[w]), dot);
+        }
+      }
     }
     const float x = dot * P.sc;
     const float mm = fmaxf(m, x);

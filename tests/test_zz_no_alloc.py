@@ -1,7 +1,8 @@
 """kvec_decode_attention_noalloc (the allocation-free decode entry point)
-against kvec_decode_attention, through the C ABI, on two calls in a row (the
-second smaller, so it reuses the start of the library's fixed scratch that
-the first left behind), and against the float64 oracle."""
+against kvec_decode_attention, through the C ABI, on several calls in a row
+(each reuses the library's fixed scratch that the calls before it left
+behind; the second call is smaller than the first), and against the float64
+oracle."""
 import sys
 
 import numpy as np
@@ -55,6 +56,16 @@ def test_noalloc_decode_matches_workspace_entry(gpu_lib):
     _case(kv, 3, 8, 4, 128, 1500, 1)   # larger first
     _case(kv, 1, 4, 7, 128, 1030, 2)   # then smaller, on the same scratch
     _case(kv, 2, 2, 2, 64, 1024, 3)
+
+
+def test_noalloc_decode_many_chunks_and_repeats(gpu_lib):
+    """One KV head over 4096 rows: 64 chunks, so the combine takes its
+    two-pass order (more chunks than one batch of loads); the same call three
+    times on the scratch the last one left behind."""
+    kv = gpu_lib
+    for rep in range(3):
+        _case(kv, 1, 1, 8, 128, 4096, 4)
+    _case(kv, 2, 1, 1, 64, 1024, 5)
 
 
 def test_noalloc_decode_rejects_plans_beyond_its_scratch(gpu_lib):
