@@ -52,14 +52,16 @@ def _elapsed(hip, a, b) -> float:
 
 
 def cpu_baseline(w, max_layers: int, min_seconds: float = 10.0):
-    """The oracle as it stands, timed on sequence 0 layer by layer in the
+    """The C++ oracle as it stands, timed on sequence 0 layer by layer in the
     step's order (layer l uses the bitmaps of layers < l), until about
-    `min_seconds` of oracle work or `max_layers` layer evictions."""
+    `min_seconds` of oracle work or `max_layers` layer evictions.  Its window
+    scores (the dominant part) run on every CPU this process may use; the
+    policy steps and the gather are single-threaded."""
     import numpy as np
-    import threadpoolctl
 
-    import oracle as orc
     import synth
+    from oracle import cxx
+    threads = cxx.default_threads()
     t_work = 0.0
     done = 0
     prev = []
@@ -71,24 +73,20 @@ def cpu_baseline(w, max_layers: int, min_seconds: float = 10.0):
         k = synth.to_f64(synth.keys(w, l, 0), w.dtype)
         v = synth.values(w, l, 0)
         t0 = time.perf_counter()
-        p, pe, imp = orc.score_layer(q, k, w.window)
-        n_t = orc.counts_from_bits(prev) if prev else np.zeros(w.seq_len, np.int64)
-        res = orc.evict_layer_from_scores(p, pe, imp, n_t, l, w)
-        orc.gather_rows(k, res.idx)
-        orc.gather_rows(v, res.idx)
+        p, pe, imp = cxx.score_layer(q, k, w.window, threads=threads)
+        n_t = cxx.counts_from_bits(prev) if prev else np.zeros(w.seq_len, np.int64)
+        res = cxx.evict_layer_from_scores(p, pe, imp, n_t, l, w)
+        cxx.gather_rows(k, res.idx)
+        cxx.gather_rows(v, res.idx)
         t_work += time.perf_counter() - t0
         prev.append(res.bits)
         done += 1
     per_layer = t_work / done
     step_s = per_layer * w.n_layers * w.batch
-    # the oracle's only parallel part is numpy's BLAS (the window products):
-    # the threads it used are that pool's size, at most the CPUs this process
-    # may run on
-    blas = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
-    host = len(os.sched_getaffinity(0))
     return {"value": w.batch * w.seq_len / step_s, "unit": "prefix tokens/s",
-            "cores": min(blas, host), "blas_threads": blas, "host_cpus": host,
-            "kind": "oracle",
+            "cores": threads, "host_cpus": len(os.sched_getaffinity(0)),
+            "kind": "oracle", "impl": "C++ (oracle/kvec_oracle.cpp), float64 window scores on "
+                                      f"{threads} threads",
             "sample": f"{done} layer evictions of sequence 0 in layer order ({t_work:.1f} s of "
                       f"oracle work, input generation excluded); per-layer time extrapolated "
                       f"to {w.n_layers} layers x batch {w.batch}"}
