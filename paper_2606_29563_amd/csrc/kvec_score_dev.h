@@ -446,6 +446,12 @@ struct ScoreTile {
   // the vector offset, which the buffer range check covers, and points keys
   // outside the tile past the end of the buffer: those read as zero without
   // touching memory, and the number of copies in flight stays the same.
+  // Pass 2's copies carry the non-temporal hint (cache-policy bit nt): in the
+  // layer pipeline they are the last reads of most of a layer's keys, and
+  // streaming them past the caches leaves more of what pass 1 read for the
+  // later stages of the pipeline (about 1.5% off the 32k step; pass 1 with
+  // the hint is 7% slower).
+  static constexpr int kCopyAux = PASS == 2 ? 2 : 0;
   __device__ __forceinline__ void dma(int u, int st) {
     auto* dst = (__attribute__((address_space(3))) char*)(reinterpret_cast<char*>(ring) + u * KR::SLOT);
     const int k0 = ks + 16 * st;
@@ -453,13 +459,13 @@ struct ScoreTile {
       const int soff = k0 * kstride;
 #pragma unroll
       for (int i = 0; i < KR::NI; ++i)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, voff[i], soff, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, voff[i], soff, 0, kCopyAux);
     } else {
 #pragma unroll
       for (int i = 0; i < KR::NI; ++i) {
         const int kk = k0 + i * KR::KPI + lane / KR::CPR;
         const int off = kk < ke ? voff[i] + k0 * kstride : kOutOfRange;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, off, 0, 0, 0);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, dst + i * 1024, 16, off, 0, 0, kCopyAux);
       }
     }
   }

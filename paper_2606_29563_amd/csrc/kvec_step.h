@@ -119,10 +119,15 @@ __device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int 
   return io;
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 // Cache store (Sec. 4.1): out[b][h][i] = K[b][h][idx[b][h][i]] (and V),
 // one 16-byte chunk per thread and round, 4 rounds per work-group; idx
 // outside [0, T) -> zeros.  All index loads are issued first, then all row
-// loads, then the stores (one memory round trip each).
+// loads, then the stores (one memory round trip each).  The row reads (the
+// last use of those rows in the step) and the stores (not read again by the
+// step) are non-temporal, so they do not displace keys that the score
+// stages read again.
 __device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b, int part) {
   constexpr int kRounds = 4;
   const Problem& P = a.P;
@@ -149,16 +154,20 @@ __device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b,
                           (int64_t)id[e] * a.ks[3]) * P.esize;
       const int64_t vo = ((int64_t)layer * a.vs[0] + (int64_t)b * a.vs[1] + (int64_t)h * a.vs[2] +
                           (int64_t)id[e] * a.vs[3]) * P.esize;
-      kv[e] = reinterpret_cast<const uint4*>(a.k + ko)[ch];
-      vv[e] = reinterpret_cast<const uint4*>(a.v + vo)[ch];
+      const u32x4 tk = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.k + ko) + ch);
+      const u32x4 tv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.v + vo) + ch);
+      kv[e] = make_uint4(tk.x, tk.y, tk.z, tk.w);
+      vv[e] = make_uint4(tv.x, tv.y, tv.z, tv.w);
     }
   }
 #pragma unroll
   for (int e = 0; e < kRounds; ++e) {
     if (ci[e] < total) {
       const int64_t o = (orow0 + ci[e] / cpr) * cpr + ci[e] % cpr;
-      reinterpret_cast<uint4*>(a.k_out)[o] = kv[e];
-      reinterpret_cast<uint4*>(a.v_out)[o] = vv[e];
+      const u32x4 tk = {kv[e].x, kv[e].y, kv[e].z, kv[e].w};
+      const u32x4 tv = {vv[e].x, vv[e].y, vv[e].z, vv[e].w};
+      __builtin_nontemporal_store(tk, reinterpret_cast<u32x4*>(a.k_out) + o);
+      __builtin_nontemporal_store(tv, reinterpret_cast<u32x4*>(a.v_out) + o);
     }
   }
 }
