@@ -388,24 +388,6 @@ struct ScoreTile {
         if (bk >= NB) mref[bk] = 0.f;  // padding blocks are never stored
       }
     } else {
-#pragma unroll
-      for (int bk = 0; bk < NB; ++bk) {
-        const int g = bk / RB, rb = bk % RB;
-        const int j = h * G + g;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = r_lo + rb * 16 + 4 * c + i;
-          // log2 of the row normaliser: from pass 1, or the caller's natural
-          // log times log2(e) (pass 2 works with base-2 exponentials)
-          const bool live = active && r >= 0;
-          float v = 0.f;
-          if (live)
-            v = io.lse_in ? io.lse_in[(int64_t)b * io.lse_b + (int64_t)j * io.lse_h + r] *
-                                1.4426950408889634f
-                          : io.lse2[((int64_t)b * P.HQ + j) * P.Wn + r];
-          nlse[bk][i] = live ? -v : -INFINITY;
-        }
-      }
       tile_base = active && r_lo + WR > base_lo;
       tile_mixed = tile_base && r_lo < base_lo;
       // A work-group exchanges importance rows when any of its tiles holds base
@@ -676,29 +658,54 @@ struct ScoreTile {
       run<false, EP>();
   }
 
+  // Pass 2: log2 of each row's normaliser, from pass 1 or the caller's
+  // natural log times log2(e) (pass 2 works with base-2 exponentials).
+  __device__ __forceinline__ void load_normalisers(float (&v)[NB][4]) {
+#pragma unroll
+    for (int bk = 0; bk < NB; ++bk) {
+      const int g = bk / RB, rb = bk % RB;
+      const int j = h * G + g;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = max(r_lo + rb * 16 + 4 * c + i, 0);
+        v[bk][i] = io.lse_in ? io.lse_in[(int64_t)b * io.lse_b + (int64_t)j * io.lse_h + r] *
+                                   1.4426950408889634f
+                             : io.lse2[((int64_t)b * P.HQ + j) * P.Wn + r];
+      }
+    }
+  }
+
   __device__ __forceinline__ void execute() {
     if (idle) {
       // no tile: only meet the work-group barrier of the write-out
       if constexpr (PASS == 2) lds_barrier();
       return;
     }
-    if constexpr (PASS == 2) {
-      // clear the running-max buffers before any head folds rows in
-      if (exch) {
-        const int nf = exchange_buffers(P.SK, P.tile2) * WR * (P.SK + 4);
-        for (int i = lane + hs * 64; i < nf; i += 64 * nh) mbuf[i] = 0.f;
-        lds_barrier();
-      }
-    }
     // Steps 0..kAhead-1 are in flight before the loop, the queries loaded
-    // right after step 0's keys (both long-latency), and step 0's fragment is
-    // read as soon as its copy and the queries have landed.
+    // right after step 0's keys (both long-latency), then pass 2's row
+    // normalisers, so that the three share one memory round trip; step 0's
+    // fragment is read as soon as all have landed.
     dma(0, 0);
     __builtin_amdgcn_sched_barrier(0);
     load_queries();
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int st = 1; st < kAhead; ++st) dma(st % KR::R, st);
+    if constexpr (PASS == 2) {
+      float v[NB][4];
+      load_normalisers(v);
+      // clear the running-max buffers before any head folds rows in
+      if (exch) {
+        const int nf = exchange_buffers(P.SK, P.tile2) * WR * (P.SK + 4);
+        for (int i = lane + hs * 64; i < nf; i += 64 * nh) mbuf[i] = 0.f;
+        lds_barrier();
+      }
+#pragma unroll
+      for (int bk = 0; bk < NB; ++bk)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          nlse[bk][i] = active && r_lo + (bk % RB) * 16 + 4 * c + i >= 0 ? -v[bk][i] : -INFINITY;
+    }
     wait_vmem<(kAhead - 1) * KR::NI>();
     read_frag<0>(0);
     if constexpr (PASS == 1) {
