@@ -227,6 +227,28 @@ kvec_status kvec_evict_model_scores(const kvec_config* cfg,
                                     uint32_t* htop_out, void* ws, size_t ws_bytes,
                                     hipStream_t stream);
 
+/* Several independent whole steps in one call: the eviction of n_steps
+ * prefills (Sec. 4.1-4.2 for each, exactly as kvec_evict_model computes it),
+ * run as one layer pipeline over their n_steps x L layers in order, so the
+ * closing launches of one step overlap the opening launches of the next
+ * (n_steps x L + 11 fused launches instead of n_steps x (L + 11)).  For
+ * throughput across back-to-back prefills; every step's outputs equal those
+ * of a kvec_evict_model call on that step's inputs.
+ *   n_steps      >= 1, n_steps x n_layers <= 2^20.
+ *   q_win, k, v  device, as kvec_evict_model with one more leading stride:
+ *                strides {step, layer, batch, head, row/t} in elements (a
+ *                step stride of 0 evicts the same prefill n_steps times).
+ *   cover_bits   device uint64 [n_steps][batch][L][ceil(T/64)].
+ *   idx          device out int32 [n_steps][L][batch][H][B].
+ *   k_out, v_out device out, contiguous [n_steps][L][batch][H][B][d].
+ * Other arguments and errors as kvec_evict_model (no profiling events). */
+kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps,
+                                   const void* q_win, const int64_t q_strides[5],
+                                   const void* k, const int64_t k_strides[5],
+                                   const void* v, const int64_t v_strides[5],
+                                   uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
+                                   void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Number of events kvec_evict_model records when given an event array
  * (n_layers + 12; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);

@@ -470,6 +470,71 @@ kvec_status kvec_evict_model_scores(const kvec_config* cfg, const void* q_win,
                      cover_bits, idx, k_out, v_out, ws, ws_bytes, stream, nullptr, &sc);
 }
 
+kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps, const void* q_win,
+                                   const int64_t q_strides[5], const void* k,
+                                   const int64_t k_strides[5], const void* v,
+                                   const int64_t v_strides[5], uint64_t* cover_bits, int32_t* idx,
+                                   void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  Geometry g;
+  kvec_status st = make_geometry(cfg, &g);
+  if (st != KVEC_OK) return st;
+  const Problem& P = g.p;
+  if (n_steps < 1 || (int64_t)n_steps * P.L > (1 << 20) || !cover_bits || !idx)
+    return KVEC_ERR_INVALID;
+  if (!q_strides || !k_strides || !v_strides) return KVEC_ERR_INVALID;
+  if (!aligned16(k) || !aligned16(v) || !strides_ok(k_strides, 5, P.esize) ||
+      !strides_ok(v_strides, 5, P.esize) || !aligned16(k_out) || !aligned16(v_out))
+    return KVEC_ERR_INVALID;
+  if (!g.keep_all && (!aligned16(q_win) || !strides_ok(q_strides, 5, P.esize)))
+    return KVEC_ERR_INVALID;
+  if (!g.keep_all && !keys_addressable(P, k_strides[4])) return KVEC_ERR_UNSUPPORTED;
+  if ((st = check_ws(g, ws, ws_bytes)) != KVEC_OK) return st;
+  // per-step output sizes (elements; words for the bitmap)
+  const int64_t bits_step = (int64_t)P.batch * P.L * P.words;
+  const int64_t idx_step = (int64_t)P.L * P.batch * P.H * P.B;
+  const int64_t out_step = idx_step * P.D;
+  if (g.keep_all) {
+    // nothing to score: each step is a keep-everything step of its own
+    for (int s = 0; s < n_steps; ++s) {
+      const char* qs = static_cast<const char*>(q_win);
+      st = kvec_evict_model(cfg, qs ? qs + (int64_t)s * q_strides[0] * P.esize : nullptr, q_strides + 1,
+                            static_cast<const char*>(k) + (int64_t)s * k_strides[0] * P.esize,
+                            k_strides + 1,
+                            static_cast<const char*>(v) + (int64_t)s * v_strides[0] * P.esize,
+                            v_strides + 1, cover_bits + s * bits_step, idx + s * idx_step,
+                            static_cast<char*>(k_out) + s * out_step * P.esize,
+                            static_cast<char*>(v_out) + s * out_step * P.esize, ws, ws_bytes, stream,
+                            nullptr);
+      if (st != KVEC_OK) return st;
+    }
+    return KVEC_OK;
+  }
+  const Workspace w = make_workspace(g);
+  ModelIO m;
+  memset(&m, 0, sizeof(m));
+  m.q = q_win;
+  m.k = k;
+  m.v = v;
+  for (int i = 0; i < 4; ++i) {
+    m.qs[i] = q_strides[i + 1];
+    m.ks[i] = k_strides[i + 1];
+    m.vs[i] = v_strides[i + 1];
+  }
+  m.bits = cover_bits;
+  m.idx = idx;
+  m.k_out = k_out;
+  m.v_out = v_out;
+  m.n_steps = n_steps;
+  m.q_step = q_strides[0];
+  m.k_step = k_strides[0];
+  m.v_step = v_strides[0];
+  m.bits_step = bits_step;
+  m.idx_step = idx_step;
+  m.out_step = out_step;
+  return dev(run_model(g, m, static_cast<char*>(ws), w, stream, nullptr));
+}
+
 kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, int32_t upto_layer,
                           int64_t* count_per_seq, hipStream_t stream) {
   Geometry g;

@@ -142,7 +142,7 @@ StepArgs base_args(const Geometry& g, char* ws, const Workspace& w) {
   a.P = g.p;
   a.w = w;
   a.ws = ws;
-  for (int s = 0; s < ST_N; ++s) a.seg[s] = Seg{-1, 0, 0};
+  for (int s = 0; s < ST_N; ++s) a.seg[s] = Seg{-1, 0, 0, 0};
   return a;
 }
 
@@ -165,6 +165,12 @@ void set_model(StepArgs& a, const ModelIO& m) {
   a.sc_pe = m.sc_pe;
   a.sc_imp = m.sc_imp;
   a.sc_htop = m.sc_htop;
+  a.q_step = m.q_step;
+  a.k_step = m.k_step;
+  a.v_step = m.v_step;
+  a.bits_step = m.bits_step;
+  a.idx_step = m.idx_step;
+  a.out_step = m.out_step;
 }
 
 hipError_t launch(const StepArgs& a, const Workspace& w, hipStream_t s) {
@@ -177,12 +183,14 @@ hipError_t launch(const StepArgs& a, const Workspace& w, hipStream_t s) {
   return hipGetLastError();
 }
 
-void set_seg(StepArgs& a, int st, int layer) {
-  if (layer < 0 || layer >= a.P.L) {
-    a.seg[st] = Seg{-1, 0, 0};
+// Stage st of pipeline layer v (layer v % L of step v / L); v outside the
+// call's n_steps x L layers leaves the stage out of the launch.
+void set_seg(StepArgs& a, int st, int v, int n_steps = 1) {
+  if (v < 0 || v >= n_steps * a.P.L) {
+    a.seg[st] = Seg{-1, 0, 0, 0};
     return;
   }
-  a.seg[st] = Seg{layer, layer % kRing, seg_count(a.P, st)};
+  a.seg[st] = Seg{v % a.P.L, v % kRing, seg_count(a.P, st), v / a.P.L};
 }
 
 hipError_t fill(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
@@ -196,8 +204,8 @@ hipError_t fill(uint32_t* p, int64_t n, uint32_t v, hipStream_t s) {
 hipError_t score_stages(StepArgs a, const Workspace& w, hipStream_t s) {
   const int order[3] = {ST_PASS1, ST_LSE, ST_PASS2};
   for (int i = a.lse ? 2 : 0; i < 3; ++i) {
-    for (int st = 0; st < ST_N; ++st) a.seg[st] = Seg{-1, 0, 0};
-    a.seg[order[i]] = Seg{0, 0, seg_count(a.P, order[i])};
+    for (int st = 0; st < ST_N; ++st) a.seg[st] = Seg{-1, 0, 0, 0};
+    a.seg[order[i]] = Seg{0, 0, seg_count(a.P, order[i]), 0};
     const hipError_t e = launch(a, w, s);
     if (e != hipSuccess) return e;
   }
@@ -243,21 +251,24 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
     if (ev) (void)hipEventRecord(ev[n_launch], s);
     return hipSuccess;
   }
-  const int n_launch = P.L + kPipeDepth;
+  // several steps: one pipeline over their n_steps x L layers in order (a
+  // layer's selection chain only links layers of its own step)
+  const int ns = m.n_steps > 0 ? m.n_steps : 1;
+  const int n_launch = ns * P.L + kPipeDepth;
   for (int j = 0; j < n_launch; ++j) {
-    set_seg(a, ST_P1B, j);
-    set_seg(a, ST_LSEB, j - 1);
-    set_seg(a, ST_P2B, j - 2);
-    set_seg(a, ST_POOLB, j - 3);
-    set_seg(a, ST_P1X, j - 4);
-    set_seg(a, ST_LSEX, j - 5);
-    set_seg(a, ST_P2X, j - 6);
-    set_seg(a, ST_POOLX, j - 7);
-    set_seg(a, ST_PREP, j - 8);
-    set_seg(a, ST_SELA, j - 9);
-    set_seg(a, ST_SELECT, j - 10);
-    set_seg(a, ST_COUNT, j - 10);
-    set_seg(a, ST_GATHER, j - 11);
+    set_seg(a, ST_P1B, j, ns);
+    set_seg(a, ST_LSEB, j - 1, ns);
+    set_seg(a, ST_P2B, j - 2, ns);
+    set_seg(a, ST_POOLB, j - 3, ns);
+    set_seg(a, ST_P1X, j - 4, ns);
+    set_seg(a, ST_LSEX, j - 5, ns);
+    set_seg(a, ST_P2X, j - 6, ns);
+    set_seg(a, ST_POOLX, j - 7, ns);
+    set_seg(a, ST_PREP, j - 8, ns);
+    set_seg(a, ST_SELA, j - 9, ns);
+    set_seg(a, ST_SELECT, j - 10, ns);
+    set_seg(a, ST_COUNT, j - 10, ns);
+    set_seg(a, ST_GATHER, j - 11, ns);
     if (ev) (void)hipEventRecord(ev[j], s);
     if ((e = launch(a, w, s)) != hipSuccess) return e;
   }
@@ -315,8 +326,8 @@ static hipError_t select_stages(const Geometry& g, int layer, const float* p_raw
   a.standalone_counts = 1;
   const int order[4] = {ST_POOL, ST_PREP, ST_SELA, ST_SELECT};
   for (int i = 0; i < 4; ++i) {
-    for (int st = 0; st < ST_N; ++st) a.seg[st] = Seg{-1, 0, 0};
-    a.seg[order[i]] = Seg{layer, 0, seg_count(P, order[i])};
+    for (int st = 0; st < ST_N; ++st) a.seg[st] = Seg{-1, 0, 0, 0};
+    a.seg[order[i]] = Seg{layer, 0, seg_count(P, order[i]), 0};
     if ((e = launch(a, w, s)) != hipSuccess) return e;
   }
   return hipSuccess;
@@ -353,7 +364,7 @@ hipError_t run_compact(const Geometry& g, int n_layers, const ModelIO& m, hipStr
   a.idx_layer_stride = (int64_t)g.p.batch * g.p.H * g.p.B;
   a.out_layer = 1;
   for (int l = 0; l < n_layers; ++l) {
-    a.seg[ST_GATHER] = Seg{l, 0, seg_count(g.p, ST_GATHER)};
+    a.seg[ST_GATHER] = Seg{l, 0, seg_count(g.p, ST_GATHER), 0};
     hipError_t e = launch(a, none, s);
     if (e != hipSuccess) return e;
   }

@@ -28,6 +28,7 @@ struct Seg {
   int layer;  // model layer the stage works on
   int slot;   // ring slot of that layer's scratch
   int count;  // tasks of this stage in the launch (work-groups: rounded up to 8)
+  int step;   // which of the call's independent steps the layer belongs to
 };
 
 struct StepArgs {
@@ -55,14 +56,16 @@ struct StepArgs {
   float* sc_imp;
   uint32_t* sc_htop;
   int standalone_counts;     // selection reads complete n_t from the counts buffer
+  // elements (words for bits) between consecutive steps of a multi-step call
+  int64_t q_step, k_step, v_step, lse_step, bits_step, idx_step, out_step;
   Seg seg[ST_N];
 };
 
-__device__ __forceinline__ ScoreIO score_io(const StepArgs& a, int layer, int slot) {
+__device__ __forceinline__ ScoreIO score_io(const StepArgs& a, int layer, int slot, int step = 0) {
   ScoreIO io;
   char* sb = a.ws + (size_t)slot * a.w.slot_bytes;
-  io.q = a.q + (int64_t)layer * a.qs[0] * a.P.esize;
-  io.k = a.k + (int64_t)layer * a.ks[0] * a.P.esize;
+  io.q = a.q + ((int64_t)step * a.q_step + (int64_t)layer * a.qs[0]) * a.P.esize;
+  io.k = a.k + ((int64_t)step * a.k_step + (int64_t)layer * a.ks[0]) * a.P.esize;
   io.qs_b = a.qs[1]; io.qs_h = a.qs[2]; io.qs_r = a.qs[3];
   io.ks_b = a.ks[1]; io.ks_h = a.ks[2]; io.ks_t = a.ks[3];
   io.lse_part = reinterpret_cast<float2*>(sb + a.w.lse_part);
@@ -70,14 +73,15 @@ __device__ __forceinline__ ScoreIO score_io(const StepArgs& a, int layer, int sl
   io.psum_base = reinterpret_cast<float*>(sb + a.w.psum_base);
   io.psum_all = reinterpret_cast<float*>(sb + a.w.psum_all);
   io.ipart = reinterpret_cast<float*>(sb + a.w.ipart);
-  io.lse_in = a.lse ? a.lse + (int64_t)layer * a.ls[0] : nullptr;
+  io.lse_in = a.lse ? a.lse + (int64_t)step * a.lse_step + (int64_t)layer * a.ls[0] : nullptr;
   io.lse_b = a.ls[1];
   io.lse_h = a.ls[2];
   return io;
 }
 
-__device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int slot) {
+__device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int slot, int step = 0) {
   SelectIO io;
+  uint64_t* const bits = a.bits + (int64_t)step * a.bits_step;
   char* sb = a.ws + (size_t)slot * a.w.slot_bytes;
   const bool standalone = a.p_raw != nullptr;
   io.psum_base = standalone ? nullptr : reinterpret_cast<const float*>(sb + a.w.psum_base);
@@ -112,10 +116,10 @@ __device__ __forceinline__ SelectIO select_io(const StepArgs& a, int layer, int 
   } else {
     // pipeline: n_t(l) = counts(l-1) + kept bit of layer l-1
     io.cnt_in = layer >= 2 ? cnt + (size_t)((layer - 1) & 1) * a.w.counts_stride : nullptr;
-    io.bits_prev = layer >= 1 ? a.bits + (int64_t)(layer - 1) * a.P.words : nullptr;
+    io.bits_prev = layer >= 1 ? bits + (int64_t)(layer - 1) * a.P.words : nullptr;
   }
-  io.bits = a.bits;
-  io.idx = a.idx + (int64_t)layer * a.idx_layer_stride;
+  io.bits = bits;
+  io.idx = a.idx + (int64_t)step * a.idx_step + (int64_t)layer * a.idx_layer_stride;
   return io;
 }
 
@@ -128,13 +132,18 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // last use of those rows in the step) and the stores (not read again by the
 // step) are non-temporal, so they do not displace keys that the score
 // stages read again.
-__device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b, int part) {
+__device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int step, int b, int part) {
   constexpr int kRounds = 4;
   const Problem& P = a.P;
   const int cpr = P.D * P.esize / 16;
   const int64_t total = (int64_t)P.H * P.B * cpr;
-  const int32_t* idx = a.idx + (int64_t)layer * a.idx_layer_stride + (int64_t)b * P.H * P.B;
+  const int32_t* idx =
+      a.idx + (int64_t)step * a.idx_step + (int64_t)layer * a.idx_layer_stride + (int64_t)b * P.H * P.B;
   const int64_t orow0 = ((int64_t)(a.out_layer ? layer : 0) * P.batch + b) * P.H * P.B;
+  const char* kin = a.k + (int64_t)step * a.k_step * P.esize;
+  const char* vin = a.v + (int64_t)step * a.v_step * P.esize;
+  char* kout = a.k_out + (int64_t)step * a.out_step * P.esize;
+  char* vout = a.v_out + (int64_t)step * a.out_step * P.esize;
   int64_t ci[kRounds];
   int id[kRounds];
 #pragma unroll
@@ -154,8 +163,8 @@ __device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b,
                           (int64_t)id[e] * a.ks[3]) * P.esize;
       const int64_t vo = ((int64_t)layer * a.vs[0] + (int64_t)b * a.vs[1] + (int64_t)h * a.vs[2] +
                           (int64_t)id[e] * a.vs[3]) * P.esize;
-      const u32x4 tk = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.k + ko) + ch);
-      const u32x4 tv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(a.v + vo) + ch);
+      const u32x4 tk = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kin + ko) + ch);
+      const u32x4 tv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vin + vo) + ch);
       kv[e] = make_uint4(tk.x, tk.y, tk.z, tk.w);
       vv[e] = make_uint4(tv.x, tv.y, tv.z, tv.w);
     }
@@ -166,8 +175,8 @@ __device__ __forceinline__ void task_gather(const StepArgs& a, int layer, int b,
       const int64_t o = (orow0 + ci[e] / cpr) * cpr + ci[e] % cpr;
       const u32x4 tk = {kv[e].x, kv[e].y, kv[e].z, kv[e].w};
       const u32x4 tv = {vv[e].x, vv[e].y, vv[e].z, vv[e].w};
-      __builtin_nontemporal_store(tk, reinterpret_cast<u32x4*>(a.k_out) + o);
-      __builtin_nontemporal_store(tv, reinterpret_cast<u32x4*>(a.v_out) + o);
+      __builtin_nontemporal_store(tk, reinterpret_cast<u32x4*>(kout) + o);
+      __builtin_nontemporal_store(tv, reinterpret_cast<u32x4*>(vout) + o);
     }
   }
 }
@@ -204,12 +213,12 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
   switch (st) {
     case ST_SELECT: {
       const int b = blk / P.H, h = blk % P.H;
-      task_select_b(P, select_io(a, sg.layer, sg.slot), sg.layer, b, h, smem);
+      task_select_b(P, select_io(a, sg.layer, sg.slot, sg.step), sg.layer, b, h, smem);
       break;
     }
     case ST_SELA: {
       const int b = blk / P.H, h = blk % P.H;
-      task_select_a(P, select_io(a, sg.layer, sg.slot), b, h, smem);
+      task_select_a(P, select_io(a, sg.layer, sg.slot, sg.step), b, h, smem);
       break;
     }
     case ST_COUNT: {
@@ -218,7 +227,8 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int layer = sg.layer;
       const uint8_t* cbase = reinterpret_cast<const uint8_t*>(a.ws + a.w.counts);
       const uint8_t* prev = layer >= 2 ? cbase + (size_t)((layer - 1) & 1) * a.w.counts_stride : nullptr;
-      const uint64_t* row = layer >= 1 ? a.bits + (int64_t)(layer - 1) * P.words : nullptr;
+      const uint64_t* row =
+          layer >= 1 ? a.bits + (int64_t)sg.step * a.bits_step + (int64_t)(layer - 1) * P.words : nullptr;
       uint8_t* out = reinterpret_cast<uint8_t*>(a.ws + a.w.counts) + (size_t)(layer & 1) * a.w.counts_stride;
       task_count(P, prev, row, out, b, blk % parts);
       break;
@@ -231,8 +241,8 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int per_b = P.n_kt1 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
       const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b) : 0u;
-      score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot), b, rem / n_rtg, rem % n_rtg,
+          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b) : 0u;
+      score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot, sg.step), b, rem / n_rtg, rem % n_rtg,
                               reinterpret_cast<float*>(smem), part, hm);
       break;
     }
@@ -243,14 +253,14 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int b = blk / per_b;
       const int rb0 = base_row_lo(P);
       const uint32_t all = (1u << P.H) - 1u;
-      const ScoreIO io = score_io(a, sg.layer, sg.slot);
+      const ScoreIO io = score_io(a, sg.layer, sg.slot, sg.step);
       if (st == ST_LSE)
         task_lse<TT, D, G>(P, io, b, blk % per_b, 0, P.Wn, all);
       else if (st == ST_LSEB)
         task_lse<TT, D, G>(P, io, b, blk % per_b, rb0, P.Wn - rb0, all);
       else
         task_lse<TT, D, G>(P, io, b, blk % per_b, 0, rb0,
-                           htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b));
+                           htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b));
       break;
     }
     case ST_PASS2:
@@ -260,9 +270,9 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
       const int per_b = P.n_kt2 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
-      const ScoreIO io = score_io(a, sg.layer, sg.slot);
+      const ScoreIO io = score_io(a, sg.layer, sg.slot, sg.step);
       const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot).stats, b) : 0u;
+          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b) : 0u;
       score_tile<TT, D, G, 2>(P, io, b, rem / n_rtg, rem % n_rtg, reinterpret_cast<float*>(smem),
                               part, hm);
       if (part != PART_EXT) {
@@ -280,7 +290,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int per_b = P.H * nt;
       const int b = blk / per_b, rem = blk % per_b;
       const int c0 = (rem % nt) * kPrepPer;
-      task_prep(P, select_io(a, sg.layer, sg.slot), sg.layer, b, rem / nt, c0,
+      task_prep(P, select_io(a, sg.layer, sg.slot, sg.step), sg.layer, b, rem / nt, c0,
                 min(P.n_prep, c0 + kPrepPer), smem);
       break;
     }
@@ -290,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int per_b = P.H * nt;
       const int b = blk / per_b, rem = blk % per_b;
       const int c0 = (rem % nt) * kPoolPer;
-      task_pool(P, select_io(a, sg.layer, sg.slot), b, rem / nt, c0, min(P.n_pool, c0 + kPoolPer),
+      task_pool(P, select_io(a, sg.layer, sg.slot, sg.step), b, rem / nt, c0, min(P.n_pool, c0 + kPoolPer),
                 smem, true, st == ST_POOL);
       break;
     }
@@ -298,7 +308,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       const int nt = (P.n_pool + kPoolPer - 1) / kPoolPer;
       const int per_b = P.delta_eff * nt;
       const int b = blk / per_b, rem = blk % per_b;
-      const SelectIO io = select_io(a, sg.layer, sg.slot);
+      const SelectIO io = select_io(a, sg.layer, sg.slot, sg.step);
       const int h = nth_bit(htop_mask(P, io.stats, b), rem / nt);
       const int c0 = (rem % nt) * kPoolPer;
       if (h >= 0) task_pool(P, io, b, h, c0, min(P.n_pool, c0 + kPoolPer), smem, false, true);
@@ -306,7 +316,7 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
     }
     case ST_GATHER: {
       const int b = blk / P.n_gather;
-      task_gather(a, sg.layer, b, blk % P.n_gather);
+      task_gather(a, sg.layer, sg.step, b, blk % P.n_gather);
       break;
     }
   }

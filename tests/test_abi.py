@@ -138,6 +138,22 @@ def test_entry_points_reject_before_launch():
     assert lib.kvec_evict_model_lse(ctypes.byref(c), fake, st4, fake, ls3, fake, ks4, fake, ks4,
                                     fake, fake, fake, fake, fake, 16, None,
                                     None) == kvec.KVEC_ERR_WORKSPACE
+    # several steps in one call: step count, outputs, strides, workspace
+    st5 = (ctypes.c_int64 * 5)(0, 32 * 64 * 128, 32 * 64 * 128, 64 * 128, 128)
+    ks5 = (ctypes.c_int64 * 5)(32 * 8 * 32768 * 128, 8 * 32768 * 128, 8 * 32768 * 128, 32768 * 128, 128)
+    steps = lib.kvec_evict_model_steps
+    for n in (0, -1, 1 << 16):
+        assert steps(ctypes.byref(c), n, fake, st5, fake, ks5, fake, ks5, fake, fake, fake, fake,
+                     fake, 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    assert steps(ctypes.byref(c), 2, fake, st5, fake, ks5, fake, ks5, None, fake, fake, fake, fake,
+                 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    assert steps(ctypes.byref(c), 2, fake, None, fake, ks5, fake, ks5, fake, fake, fake, fake, fake,
+                 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    bad5 = (ctypes.c_int64 * 5)(3, 8 * 32768 * 128, 8 * 32768 * 128, 32768 * 128, 128)
+    assert steps(ctypes.byref(c), 2, fake, st5, fake, bad5, fake, ks5, fake, fake, fake, fake, fake,
+                 1 << 40, None) == kvec.KVEC_ERR_INVALID
+    assert steps(ctypes.byref(c), 2, fake, st5, fake, ks5, fake, ks5, fake, fake, fake, fake, fake,
+                 16, None) == kvec.KVEC_ERR_WORKSPACE
 
 
 def test_decode_validation():
