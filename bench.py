@@ -249,6 +249,89 @@ def copy_calibration(mib: int) -> None:
     print(json.dumps({"copy_calibration_bytes": n, "copies": 3}))
 
 
+def gen_inputs(w, dev, dt, n_gen=None):
+    """Device tensors q [L][b][HQ][O'][d], k and v [L][b][H][T][d] of a synthetic
+    workload.  With n_gen < L only layers 0..n_gen-1 are generated and layer l
+    holds a copy of layer l % n_gen (separate device memory)."""
+    import torch
+
+    import synth
+    L, b, H, HQ, T, d = w.n_layers, w.batch, w.n_kv_heads, w.n_q_heads, w.seq_len, w.head_dim
+    n_gen = L if n_gen is None else min(n_gen, L)
+    q = torch.empty((L, b, HQ, w.rows, d), dtype=dt, device=dev)
+    k = torch.empty((L, b, H, T, d), dtype=dt, device=dev)
+    v = torch.empty_like(k)
+    for l in range(n_gen):
+        for s in range(b):
+            for dst, arr in ((q, synth.queries(w, l, s)), (k, synth.keys(w, l, s)),
+                             (v, synth.values(w, l, s))):
+                t = torch.from_numpy(arr)
+                if w.dtype == "bf16":
+                    t = t.view(torch.bfloat16)
+                dst[l, s].copy_(t)
+    for l in range(n_gen, L):
+        for x in (q, k, v):
+            x[l].copy_(x[l % n_gen])
+    return q, k, v
+
+
+def measure_other(wi, args, hip, stream):
+    """One more workload, timed like the headline: the isolated step (K steps,
+    one call each) and K pipelined steps in one call.  The fractions are the
+    step's algorithmic bytes and flops (as for the headline) over the step's
+    GPU time between HIP events."""
+    import torch
+
+    import synth
+    from paper_2606_29563_amd import kvec
+    w = synth.workload(wi)
+    dev = torch.device("cuda:0")
+    dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    L, b, H, HQ, T, d, B = (w.n_layers, w.batch, w.n_kv_heads, w.n_q_heads, w.seq_len,
+                            w.head_dim, w.budget)
+    # the large prefixes generate 4 layers and repeat them (the step's cost does
+    # not depend on which layer's values it reads, only on their distribution)
+    n_gen = L if b * T <= 32768 else 4
+    print(f"[bench] other workload {w.name}: generating {n_gen} of {L} layers", file=sys.stderr,
+          flush=True)
+    q, k, v = gen_inputs(w, dev, dt, n_gen)
+    cfg = kvec.Config.from_workload(w)
+    ws = torch.empty(kvec.kvec_workspace_size(cfg), dtype=torch.uint8, device=dev)
+    bits = torch.empty((b, L, (T + 63) // 64), dtype=torch.int64, device=dev)
+    idx = torch.empty((L, b, H, B), dtype=torch.int32, device=dev)
+    ko = torch.empty((L, b, H, B, d), dtype=dt, device=dev)
+    vo = torch.empty_like(ko)
+    es = 2 if w.dtype == "bf16" else 4
+    step_bytes = L * b * (H * T * d * es + HQ * w.rows * d * es + 4 * H * B * d * es)
+    O, Wn, delta = w.window, w.rows, w.n_adjust_heads if w.rows > w.window else 0
+    step_flops = 2 * d * L * b * (HQ * O * T + (HQ // H) * delta * (Wn - O) * T)
+    durs, wall = time_steps(hip, stream,
+                            lambda: kvec.kvec_evict_model(cfg, q, k, v, bits, idx, ko, vo, ws),
+                            args.steps, args.warmup)
+    ms = wall / args.steps
+    ms_gpu = sum(durs) / len(durs)
+    n = max(2, args.steps)
+    bn = torch.empty((n,) + tuple(bits.shape), dtype=bits.dtype, device=dev)
+    iN = torch.empty((n,) + tuple(idx.shape), dtype=idx.dtype, device=dev)
+    kon = torch.empty((n,) + tuple(ko.shape), dtype=ko.dtype, device=dev)
+    von = torch.empty_like(kon)
+    qn, kn, vn = (x.unsqueeze(0).expand(n, *x.shape) for x in (q, k, v))
+    durs, _ = time_steps(hip, stream,
+                         lambda: kvec.kvec_evict_model_steps(cfg, qn, kn, vn, bn, iN, kon, von, ws), 2, 1)
+    assert all(torch.equal(iN[i], idx) for i in range(n)), "pipelined steps differ"
+    ms_pipe = sum(durs) / len(durs) / n
+    out = {"workload": w.name, "layers": L, "batch": b, "kv_heads": H, "q_heads": HQ,
+           "seq_len": T, "budget": B, "generated_layers": n_gen, "ms_per_step": round(ms, 4),
+           "value": round(b * T / (ms * 1e-3), 1), "unit": "prefix tokens/s",
+           "hbm_frac": round(step_bytes / (ms_gpu * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "mfma_frac": round(step_flops / (ms_gpu * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+           "pipelined_ms_per_step": round(ms_pipe, 4),
+           "pipelined_value": round(b * T / (ms_pipe * 1e-3), 1)}
+    print(f"[bench] {w.name}: {ms:.4f} ms per step, pipelined {ms_pipe:.4f}", file=sys.stderr,
+          flush=True)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -266,6 +349,10 @@ def main():
                          "kvec_select_cover, kvec_compact) one by one, each timed on its own")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--other-workloads", default=None, metavar="LIST",
+                    help="comma-separated workload indices also measured (isolated and "
+                         "pipelined step) and reported under other_workloads; default 1,3,4,5 "
+                         "for the headline run, empty to skip")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU; multi-GPU runs are not part of this build "
@@ -288,17 +375,7 @@ def main():
     L, b, H, HQ, T, d, B = (w.n_layers, w.batch, w.n_kv_heads, w.n_q_heads, w.seq_len,
                             w.head_dim, w.budget)
     print(f"[bench] {w.name}: generating {L} layers of inputs", file=sys.stderr, flush=True)
-    q = torch.empty((L, b, HQ, w.rows, d), dtype=dt, device=dev)
-    k = torch.empty((L, b, H, T, d), dtype=dt, device=dev)
-    v = torch.empty_like(k)
-    for l in range(L):
-        for s in range(b):
-            for dst, arr in ((q, synth.queries(w, l, s)), (k, synth.keys(w, l, s)),
-                             (v, synth.values(w, l, s))):
-                t = torch.from_numpy(arr)
-                if w.dtype == "bf16":
-                    t = t.view(torch.bfloat16)
-                dst[l, s].copy_(t)
+    q, k, v = gen_inputs(w, dev, dt)
     cfg = kvec.Config.from_workload(w)
     ws = torch.empty(kvec.kvec_workspace_size(cfg), dtype=torch.uint8, device=dev)
     bits = torch.empty((b, L, (T + 63) // 64), dtype=torch.int64, device=dev)
@@ -496,6 +573,20 @@ def main():
             steps_obj = {"entry": "kvec_evict_model_steps", "error": repr(e)}
             print(f"[bench] pipelined steps failed: {e!r}", file=sys.stderr, flush=True)
 
+    others = None
+    ow = args.other_workloads
+    if ow is None:
+        ow = "1,3,4,5" if (args.workload == 2 and args.path == "both") else ""
+    if ow:
+        others = []
+        for wi in [int(x) for x in ow.split(",") if x.strip()]:
+            try:
+                others.append(measure_other(wi, args, hip, stream))
+            except Exception as e:  # the headline line must not depend on this extra
+                others.append({"workload_index": wi, "error": repr(e)})
+                print(f"[bench] workload {wi} failed: {e!r}", file=sys.stderr, flush=True)
+            torch.cuda.empty_cache()
+
     cpu = None
     if not args.no_cpu_baseline:
         # layers of sequence 0 in order until about 10 s of oracle work
@@ -523,6 +614,8 @@ def main():
         out["prefill_lse_step"] = lse_obj
     if steps_obj is not None:
         out["pipelined_steps"] = steps_obj
+    if others is not None:
+        out["other_workloads"] = others
     if dec_obj is not None:
         out["decode_attention"] = dec_obj
     print(json.dumps(out))
