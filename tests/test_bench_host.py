@@ -35,3 +35,24 @@ def test_algorithmic_bytes_per_token_at_32k():
     L, b, H, HQ, T, d, B, Wn, es = 32, 1, 8, 32, 32768, 128, 1024, 64, 2
     step = L * b * (H * T * d * es + HQ * Wn * d * es + 4 * H * B * d * es)
     assert step // T == 74240
+
+
+def test_repeated_layers_are_copies_of_the_generated_ones():
+    # the other-workload leg generates n_gen layers and repeats them; every
+    # layer is its own memory and equals the generated layer l % n_gen
+    import numpy as np
+    import torch
+
+    import synth
+    w = synth.workload(0)
+    dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    q, k, v = bench.gen_inputs(w, torch.device("cpu"), dt, n_gen=1)
+    assert q.shape[0] == k.shape[0] == v.shape[0] == w.n_layers >= 2
+    for x in (q, k, v):
+        assert x[1].data_ptr() != x[0].data_ptr()
+        assert torch.equal(x[1], x[0])
+    k0 = synth.keys(w, 0, 0)
+    got = k[0, 0].numpy() if dt == torch.float32 else k[0, 0].view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got, k0)
+    q2, k2, _ = bench.gen_inputs(w, torch.device("cpu"), dt)
+    assert torch.equal(k2[0], k[0]) and not torch.equal(k2[1], k2[0])
