@@ -249,6 +249,22 @@ kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps,
                                    uint64_t* cover_bits, int32_t* idx, void* k_out, void* v_out,
                                    void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Several steps, as kvec_evict_model_steps, with every step's window-row
+ * normalisers from the caller, as kvec_evict_model_lse (Sec. 5.1).
+ *   lse          device, fp32 [n_steps][L][batch][n_q_heads][O'] with strides
+ *                lse_strides = {step, layer, batch, head} in elements (any
+ *                non-negative values, 0 included), rows contiguous.  Required
+ *                even when T <= B (then unread).
+ * Other arguments, outputs and errors as kvec_evict_model_steps. */
+kvec_status kvec_evict_model_lse_steps(const kvec_config* cfg, int32_t n_steps,
+                                       const void* q_win, const int64_t q_strides[5],
+                                       const float* lse, const int64_t lse_strides[4],
+                                       const void* k, const int64_t k_strides[5],
+                                       const void* v, const int64_t v_strides[5],
+                                       uint64_t* cover_bits, int32_t* idx, void* k_out,
+                                       void* v_out, void* ws, size_t ws_bytes,
+                                       hipStream_t stream);
+
 /* Number of events kvec_evict_model records when given an event array
  * (n_layers + 12; 0 when T <= B), or -1 for an invalid configuration. */
 int32_t kvec_profile_points(const kvec_config* cfg);

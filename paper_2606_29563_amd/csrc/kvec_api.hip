@@ -470,12 +470,16 @@ kvec_status kvec_evict_model_scores(const kvec_config* cfg, const void* q_win,
                      cover_bits, idx, k_out, v_out, ws, ws_bytes, stream, nullptr, &sc);
 }
 
-kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps, const void* q_win,
-                                   const int64_t q_strides[5], const void* k,
-                                   const int64_t k_strides[5], const void* v,
-                                   const int64_t v_strides[5], uint64_t* cover_bits, int32_t* idx,
-                                   void* k_out, void* v_out, void* ws, size_t ws_bytes,
-                                   hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// n_steps independent steps in one pipeline (lse null: the two-pass path).
+kvec_status evict_steps(const kvec_config* cfg, int32_t n_steps, const void* q_win,
+                        const int64_t q_strides[5], const float* lse, const int64_t lse_strides[4],
+                        const void* k, const int64_t k_strides[5], const void* v,
+                        const int64_t v_strides[5], uint64_t* cover_bits, int32_t* idx,
+                        void* k_out, void* v_out, void* ws, size_t ws_bytes, hipStream_t stream) {
   Geometry g;
   kvec_status st = make_geometry(cfg, &g);
   if (st != KVEC_OK) return st;
@@ -521,6 +525,11 @@ kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps, cons
     m.ks[i] = k_strides[i + 1];
     m.vs[i] = v_strides[i + 1];
   }
+  if (lse) {
+    m.lse = lse;
+    for (int i = 0; i < 3; ++i) m.ls[i] = lse_strides[i + 1];
+    m.lse_step = lse_strides[0];
+  }
   m.bits = cover_bits;
   m.idx = idx;
   m.k_out = k_out;
@@ -533,6 +542,32 @@ kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps, cons
   m.idx_step = idx_step;
   m.out_step = out_step;
   return dev(run_model(g, m, static_cast<char*>(ws), w, stream, nullptr));
+}
+
+}  // namespace
+
+extern "C" {
+
+kvec_status kvec_evict_model_steps(const kvec_config* cfg, int32_t n_steps, const void* q_win,
+                                   const int64_t q_strides[5], const void* k,
+                                   const int64_t k_strides[5], const void* v,
+                                   const int64_t v_strides[5], uint64_t* cover_bits, int32_t* idx,
+                                   void* k_out, void* v_out, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  return evict_steps(cfg, n_steps, q_win, q_strides, nullptr, nullptr, k, k_strides, v, v_strides,
+                     cover_bits, idx, k_out, v_out, ws, ws_bytes, stream);
+}
+
+kvec_status kvec_evict_model_lse_steps(const kvec_config* cfg, int32_t n_steps, const void* q_win,
+                                       const int64_t q_strides[5], const float* lse,
+                                       const int64_t lse_strides[4], const void* k,
+                                       const int64_t k_strides[5], const void* v,
+                                       const int64_t v_strides[5], uint64_t* cover_bits,
+                                       int32_t* idx, void* k_out, void* v_out, void* ws,
+                                       size_t ws_bytes, hipStream_t stream) {
+  if (!lse_ok(lse, lse_strides, 4)) return KVEC_ERR_INVALID;
+  return evict_steps(cfg, n_steps, q_win, q_strides, lse, lse_strides, k, k_strides, v, v_strides,
+                     cover_bits, idx, k_out, v_out, ws, ws_bytes, stream);
 }
 
 kvec_status kvec_coverage(const kvec_config* cfg, const uint64_t* cover_bits, int32_t upto_layer,

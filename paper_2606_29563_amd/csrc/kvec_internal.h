@@ -120,7 +120,7 @@ struct ModelIO {
   // independent steps run as one pipeline over n_steps x L layers; elements
   // (words for bits) between consecutive steps of each tensor
   int n_steps;
-  int64_t q_step, k_step, v_step, bits_step, idx_step, out_step;
+  int64_t q_step, k_step, v_step, lse_step, bits_step, idx_step, out_step;
 };
 
 hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Workspace& w,

@@ -168,6 +168,7 @@ void set_model(StepArgs& a, const ModelIO& m) {
   a.q_step = m.q_step;
   a.k_step = m.k_step;
   a.v_step = m.v_step;
+  a.lse_step = m.lse_step;
   a.bits_step = m.bits_step;
   a.idx_step = m.idx_step;
   a.out_step = m.out_step;
@@ -231,29 +232,29 @@ hipError_t run_model(const Geometry& g, const ModelIO& m, char* ws, const Worksp
   a.idx_layer_stride = (int64_t)P.batch * P.H * P.B;
   a.out_layer = 1;
   a.standalone_counts = 0;
+  // several steps: one pipeline over their n_steps x L layers in order (a
+  // layer's selection chain only links layers of its own step)
+  const int ns = m.n_steps > 0 ? m.n_steps : 1;
   if (m.lse) {
     // The row normalisers come from the caller (the log-sum-exp of the
-    // layer's prefill attention): no pass 1, a 6-launch pipeline.
-    const int n_launch = P.L + kPipeDepthLse;
+    // layer's prefill attention): no pass 1, a shorter pipeline.
+    const int n_launch = ns * P.L + kPipeDepthLse;
     for (int j = 0; j < n_launch; ++j) {
-      set_seg(a, ST_P2B, j);
-      set_seg(a, ST_POOLB, j - 1);
-      set_seg(a, ST_P2X, j - 2);
-      set_seg(a, ST_POOLX, j - 3);
-      set_seg(a, ST_PREP, j - 4);
-      set_seg(a, ST_SELA, j - 5);
-      set_seg(a, ST_SELECT, j - 6);
-      set_seg(a, ST_COUNT, j - 6);
-      set_seg(a, ST_GATHER, j - 7);
+      set_seg(a, ST_P2B, j, ns);
+      set_seg(a, ST_POOLB, j - 1, ns);
+      set_seg(a, ST_P2X, j - 2, ns);
+      set_seg(a, ST_POOLX, j - 3, ns);
+      set_seg(a, ST_PREP, j - 4, ns);
+      set_seg(a, ST_SELA, j - 5, ns);
+      set_seg(a, ST_SELECT, j - 6, ns);
+      set_seg(a, ST_COUNT, j - 6, ns);
+      set_seg(a, ST_GATHER, j - 7, ns);
       if (ev) (void)hipEventRecord(ev[j], s);
       if ((e = launch(a, w, s)) != hipSuccess) return e;
     }
     if (ev) (void)hipEventRecord(ev[n_launch], s);
     return hipSuccess;
   }
-  // several steps: one pipeline over their n_steps x L layers in order (a
-  // layer's selection chain only links layers of its own step)
-  const int ns = m.n_steps > 0 ? m.n_steps : 1;
   const int n_launch = ns * P.L + kPipeDepth;
   for (int j = 0; j < n_launch; ++j) {
     set_seg(a, ST_P1B, j, ns);

@@ -88,6 +88,7 @@ _lib = None
 EXPORTS = ["kvec_workspace_size", "kvec_score", "kvec_score_lse", "kvec_select_cover",
            "kvec_compact", "kvec_evict_layer", "kvec_evict_model", "kvec_evict_model_lse",
            "kvec_evict_layer_lse", "kvec_evict_model_scores", "kvec_evict_model_steps",
+           "kvec_evict_model_lse_steps",
            "kvec_profile_points", "kvec_profile_points_lse", "kvec_coverage",
            "kvec_decode_workspace_size", "kvec_decode_attention", "kvec_decode_attention_noalloc",
            "kvec_status_string"]
@@ -121,6 +122,8 @@ def load() -> ctypes.CDLL:
                                             vp, vp, vp, vp, sz, vp]
     lib.kvec_evict_model_steps.argtypes = [P, i32, vp, I64x, vp, I64x, vp, I64x, vp, vp, vp, vp, vp,
                                            sz, vp]
+    lib.kvec_evict_model_lse_steps.argtypes = [P, i32, vp, I64x, vp, I64x, vp, I64x, vp, I64x, vp, vp,
+                                               vp, vp, vp, sz, vp]
     lib.kvec_decode_attention_noalloc.argtypes = [P, vp, I64x, vp, vp, I64x, i32, vp, vp, vp]
     lib.kvec_coverage.argtypes = [P, vp, i32, vp, vp]
     lib.kvec_decode_workspace_size.argtypes = [P, i32, ctypes.POINTER(sz)]
@@ -250,6 +253,20 @@ def kvec_evict_model_steps(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_o
                                          _ptr(idx), _ptr(k_out), _ptr(v_out), _ptr(ws),
                                          ws.numel() * ws.element_size(), _stream(stream)),
            "kvec_evict_model_steps")
+
+
+def kvec_evict_model_lse_steps(cfg: Config, q_win, lse, k, v, cover_bits, idx, k_out, v_out, ws,
+                               stream=None) -> None:
+    """As kvec_evict_model_steps, with the window rows' natural-log normalisers
+    lse fp32 [n][L][b][HQ][O'] (any leading strides, rows contiguous)."""
+    c = cfg.c()
+    n = k.shape[0]
+    _check(load().kvec_evict_model_lse_steps(ctypes.byref(c), n, _ptr(q_win), _strides(q_win, 5),
+                                             _ptr(lse), _lse_strides(lse, 4), _ptr(k), _strides(k, 5),
+                                             _ptr(v), _strides(v, 5), _ptr(cover_bits), _ptr(idx),
+                                             _ptr(k_out), _ptr(v_out), _ptr(ws),
+                                             ws.numel() * ws.element_size(), _stream(stream)),
+           "kvec_evict_model_lse_steps")
 
 
 def kvec_evict_model_scores(cfg: Config, q_win, k, v, cover_bits, idx, k_out, v_out, p_raw_out,

@@ -154,6 +154,18 @@ def test_entry_points_reject_before_launch():
                  1 << 40, None) == kvec.KVEC_ERR_INVALID
     assert steps(ctypes.byref(c), 2, fake, st5, fake, ks5, fake, ks5, fake, fake, fake, fake, fake,
                  16, None) == kvec.KVEC_ERR_WORKSPACE
+    # ... with the normalisers given: the lse pointer and strides are checked first
+    ls4 = (ctypes.c_int64 * 4)(0, 32 * 64, 32 * 64, 64)
+    lsteps = lib.kvec_evict_model_lse_steps
+    def lcall(n=2, lse=fake, lstr=ls4, ws_bytes=1 << 40):
+        return lsteps(ctypes.byref(c), n, fake, st5, lse, lstr, fake, ks5, fake, ks5, fake, fake, fake,
+                      fake, fake, ws_bytes, None)
+    assert lcall(lse=None) == kvec.KVEC_ERR_INVALID
+    assert lcall(lse=ctypes.c_void_p((1 << 20) + 2)) == kvec.KVEC_ERR_INVALID
+    assert lcall(lstr=None) == kvec.KVEC_ERR_INVALID
+    assert lcall(lstr=(ctypes.c_int64 * 4)(-1, 32 * 64, 32 * 64, 64)) == kvec.KVEC_ERR_INVALID
+    assert lcall(n=0) == kvec.KVEC_ERR_INVALID
+    assert lcall(ws_bytes=16) == kvec.KVEC_ERR_WORKSPACE
 
 
 def test_decode_validation():

@@ -1,11 +1,12 @@
-"""kvec_evict_model_steps: several independent steps in one pipelined call.
+"""kvec_evict_model_steps and kvec_evict_model_lse_steps: several independent
+steps in one pipelined call.
 
 Every step's outputs (bitmap rows, indices, kept K and V) must be
-bit-identical to a kvec_evict_model call on that step's inputs, with layer
-counts below and above the pipeline depth (so that up to several steps share
-a launch), distinct inputs per step, and a step stride of 0 (one prefill
-evicted repeatedly).  The single-step path is checked against the oracle
-elsewhere; this pins the multi-step plumbing to it.
+bit-identical to a kvec_evict_model (kvec_evict_model_lse) call on that step's
+inputs, with layer counts below and above the pipeline depth (so that up to
+several steps share a launch), distinct inputs per step, and a step stride of
+0 (one prefill evicted repeatedly).  The single-step paths are checked against
+the oracle elsewhere; this pins the multi-step plumbing to them.
 """
 import sys
 
@@ -13,6 +14,7 @@ import pytest
 
 import synth
 from kvec_testlib import model_tensors
+from test_gpu_parity import oracle_lse_tensor
 
 pytestmark = pytest.mark.gpu
 
@@ -35,27 +37,31 @@ def _outs(kv, w, n):
     return bits, idx, ko, torch.zeros_like(ko)
 
 
-def _check(kv, ws_list, n_steps, shared):
+def _check(kv, ws_list, n_steps, shared, lse=False):
     import torch
     w0 = ws_list[0]
     cfg = kv.Config.from_workload(w0)
     ws = torch.empty(kv.kvec_workspace_size(cfg), dtype=torch.uint8, device="cuda")
-    ins = [model_tensors(w) for w in ws_list]
+    ins = [model_tensors(w) + ((oracle_lse_tensor(w),) if lse else ()) for w in ws_list]
     if shared:
-        q = ins[0][0].unsqueeze(0).expand(n_steps, *ins[0][0].shape)
-        k = ins[0][1].unsqueeze(0).expand(n_steps, *ins[0][1].shape)
-        v = ins[0][2].unsqueeze(0).expand(n_steps, *ins[0][2].shape)
+        stacked = [x.unsqueeze(0).expand(n_steps, *x.shape) for x in ins[0]]
         ins = [ins[0]] * n_steps
     else:
-        q = torch.stack([x[0] for x in ins])
-        k = torch.stack([x[1] for x in ins])
-        v = torch.stack([x[2] for x in ins])
+        stacked = [torch.stack([x[i] for x in ins]) for i in range(len(ins[0]))]
     bits, idx, ko, vo = _outs(kv, w0, n_steps)
-    kv.kvec_evict_model_steps(cfg, q, k, v, bits, idx, ko, vo, ws)
+    if lse:
+        q, k, v, ls = stacked
+        kv.kvec_evict_model_lse_steps(cfg, q, ls, k, v, bits, idx, ko, vo, ws)
+    else:
+        q, k, v = stacked
+        kv.kvec_evict_model_steps(cfg, q, k, v, bits, idx, ko, vo, ws)
     torch.cuda.synchronize()
     for s in range(n_steps):
         b1, i1, k1, v1 = (x[0] for x in _outs(kv, w0, 1))
-        kv.kvec_evict_model(cfg, ins[s][0], ins[s][1], ins[s][2], b1, i1, k1, v1, ws)
+        if lse:
+            kv.kvec_evict_model_lse(cfg, ins[s][0], ins[s][3], ins[s][1], ins[s][2], b1, i1, k1, v1, ws)
+        else:
+            kv.kvec_evict_model(cfg, ins[s][0], ins[s][1], ins[s][2], b1, i1, k1, v1, ws)
         torch.cuda.synchronize()
         assert torch.equal(bits[s], b1), f"step {s}: bitmap rows differ"
         assert torch.equal(idx[s], i1), f"step {s}: indices differ"
@@ -80,3 +86,20 @@ def test_steps_keep_everything(gpu_lib):
     _say("[steps] T <= B: keep everything")
     w = _wl(3, 60, T=150, B=200)
     _check(gpu_lib, [w, _wl(3, 61, T=150, B=200)], 2, shared=False)
+
+
+@pytest.mark.parametrize("L", [3, 10])
+def test_lse_steps_match_single_calls(gpu_lib, L):
+    n = 3
+    _say(f"[steps-lse] L={L} n={n}, distinct inputs and normalisers")
+    _check(gpu_lib, [_wl(L, 70 + s) for s in range(n)], n, shared=False, lse=True)
+
+
+def test_lse_steps_shared_prefill(gpu_lib):
+    _say("[steps-lse] L=5 n=3, step stride 0")
+    _check(gpu_lib, [_wl(5, 80)], 3, shared=True, lse=True)
+
+
+def test_lse_steps_keep_everything(gpu_lib):
+    _say("[steps-lse] T <= B: keep everything")
+    _check(gpu_lib, [_wl(2, 90, T=150, B=200), _wl(2, 91, T=150, B=200)], 2, shared=False, lse=True)
