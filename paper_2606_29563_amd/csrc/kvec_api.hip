@@ -83,12 +83,11 @@ kvec_status make_geometry(const kvec_config* c, Geometry* g) {
   // remaining extended-window rows for the delta_eff heads of H_top
   x.n_rtg_base = (x.n_rt_base + tpw - 1) / tpw;
   const int n_rt_ext = x.n_rt - x.n_rt_base;
-  x.tpw_x = x.delta_eff > 0 ? 8 / x.delta_eff : 0;
-  x.n_rtg_x = x.delta_eff > 0 && n_rt_ext > 0 ? (n_rt_ext + x.tpw_x - 1) / x.tpw_x : 0;
+  x.n_rt_x = x.delta_eff > 0 && n_rt_ext > 0 ? n_rt_ext : 0;
   auto lds_p2 = [&](int sk, int tile) {
     const size_t all = (size_t)tpw * p2_slot_floats(H, x.WR, sk, tile, H > 1, x.nsum);
-    const size_t ext =
-        x.delta_eff > 0 ? (size_t)x.tpw_x * p2_slot_floats(x.delta_eff, x.WR, sk, tile, false, x.nsum) : 0;
+    // EXT passes: one task per wave, each wave its own slot of one head
+    const size_t ext = x.n_rt_x > 0 ? (size_t)8 * p2_slot_floats(1, x.WR, sk, tile, false, x.nsum) : 0;
     return ring + (all > ext ? all : ext) * 4;
   };
   const size_t lds_cap = kLdsMax - kLdsStatic;
@@ -153,8 +152,7 @@ Workspace make_workspace(const Geometry& g) {
   // dynamic LDS: the largest task
   const int tpw = 8 / P.H;
   const size_t p2_all = (size_t)tpw * p2_slot_floats(P.H, P.WR, P.SK, P.tile2, P.H > 1, P.nsum);
-  const size_t p2_ext =
-      P.delta_eff > 0 ? (size_t)P.tpw_x * p2_slot_floats(P.delta_eff, P.WR, P.SK, P.tile2, false, P.nsum) : 0;
+  const size_t p2_ext = P.n_rt_x > 0 ? (size_t)8 * p2_slot_floats(1, P.WR, P.SK, P.tile2, false, P.nsum) : 0;
   const size_t lds_p2 = key_ring_bytes(P.esize, P.D) + (p2_all > p2_ext ? p2_all : p2_ext) * 4;
   const size_t lds_pool = (size_t)(2 * (kPoolPer * kPoolChunk + 64) + 2 * kHistBins) * 4 + kPoolPer * 16;
   const size_t lds_prep = 256;

@@ -70,8 +70,8 @@ struct Problem {
   int nsum;        // pass-2 per-key sums per head: 1 when O is a multiple of WR (no row
                    // tile holds both last-O and earlier rows), else 2
   int n_rtg_base;  // work-groups per key tile of a BASE pass (8/H row tiles each)
-  int tpw_x;       // row tiles per work-group of an EXT pass (8 / delta_eff)
-  int n_rtg_x;     // work-groups per key tile of an EXT pass (0: no EXT pass)
+  int n_rt_x;      // row tiles of an EXT pass (extended-window rows only; 0: no EXT
+                   // pass); its tasks (key tile, H_top head, row tile) go one per wave
   int n_pool, n_prep, words;
   int esize;
   int n_gather;  // gather work-groups per (layer, sequence)

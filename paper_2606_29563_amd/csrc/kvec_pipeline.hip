@@ -107,6 +107,12 @@ __global__ void coverage_kernel(const uint64_t* bits, int64_t* count, int L, int
   }
 }
 
+// Work-groups of an EXT pass over n_kt key tiles: its (sequence, key tile,
+// H_top head, row tile) tasks packed eight to a work-group, one per wave.
+int ext_wgs(const Problem& P, int n_kt) {
+  return P.n_rt_x ? (int)(((int64_t)P.batch * n_kt * P.delta_eff * P.n_rt_x + 7) / 8) : 0;
+}
+
 int seg_count(const Problem& P, int st) {
   const bool ext = P.delta_eff > 0;
   switch (st) {
@@ -115,13 +121,13 @@ int seg_count(const Problem& P, int st) {
     case ST_COUNT: return P.batch * ((P.words + kCountWords - 1) / kCountWords);
     case ST_PASS1: return P.batch * P.n_kt1 * P.n_rtg;
     case ST_P1B: return P.batch * P.n_kt1 * P.n_rtg_base;
-    case ST_P1X: return P.batch * P.n_kt1 * P.n_rtg_x;
+    case ST_P1X: return ext_wgs(P, P.n_kt1);
     case ST_LSE:
     case ST_LSEB: return P.batch * lse_tasks_per_seq(P, st);
-    case ST_LSEX: return P.n_rtg_x ? P.batch * lse_tasks_per_seq(P, st) : 0;
+    case ST_LSEX: return P.n_rt_x ? P.batch * lse_tasks_per_seq(P, st) : 0;
     case ST_PASS2: return P.batch * P.n_kt2 * P.n_rtg;
     case ST_P2B: return P.batch * P.n_kt2 * P.n_rtg_base;
-    case ST_P2X: return P.batch * P.n_kt2 * P.n_rtg_x;
+    case ST_P2X: return ext_wgs(P, P.n_kt2);
     case ST_POOL:
     case ST_POOLB: return P.batch * P.H * ((P.n_pool + kPoolPer - 1) / kPoolPer);
     case ST_POOLX: return ext ? P.batch * P.delta_eff * ((P.n_pool + kPoolPer - 1) / kPoolPer) : 0;

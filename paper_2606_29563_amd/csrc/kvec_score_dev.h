@@ -327,7 +327,11 @@ struct ScoreTile {
   float lsum[NBP][4], nlse[NB][4];
   int pos[RB][4];
 
-  // part: which row tiles and heads (PART_EXT: the heads set in hmask).
+  // part: which row tiles and heads.  ALL and BASE: wave w takes head
+  // w % H of row tile rtg * (8 / H) + w / H (with H not dividing 8 the last
+  // waves are idle).  EXT: every wave has a task of its own, given by the
+  // caller (b, kt and rtg may differ between the waves): hmask holds its one
+  // head (0: no task) and rtg its extended-window row tile.
   __device__ __forceinline__ ScoreTile(const Problem& P_, const ScoreIO& io_, int b_, int kt_,
                                        int rtg_, float* smem, Part part, uint32_t hmask)
       : P(P_), io(io_), b(b_), kt(kt_), rtg(rtg_) {
@@ -337,17 +341,16 @@ struct ScoreTile {
     lane = threadIdx.x & 63;
     c = lane >> 4;
     n = lane & 15;
-    // wave w: head hs of the pass's nh heads, row tile slot w / nh; with
-    // nh not dividing 8 the last waves are idle
-    nh = part == PART_EXT ? __popc(hmask) : P.H;
+    const bool ext = part == PART_EXT;
+    nh = ext ? 1 : P.H;
     tpw = 8 / nh;
     hs = w % nh;
     slot = w / nh;
-    idle = slot >= tpw;
-    h = part == PART_EXT ? nth_bit(hmask, hs) : hs;
-    const int rt0 = part == PART_EXT ? P.n_rt_base : 0;
+    idle = ext ? hmask == 0u : slot >= tpw;
+    h = ext ? (hmask ? (int)__builtin_ctz(hmask) : 0) : hs;
+    const int rt0 = ext ? P.n_rt_base : 0;
     const int rt_end = part == PART_BASE ? P.n_rt_base : P.n_rt;
-    rt = rt0 + rtg * tpw + slot;
+    rt = ext ? rt0 + rtg : rt0 + rtg * tpw + slot;
     active = !idle && rt < rt_end;
     r_lo = P.Wn - (rt + 1) * WR;  // lowest window row of this tile (may be < 0)
     base_lo = P.Wn - P.O;         // first row of the last-O window

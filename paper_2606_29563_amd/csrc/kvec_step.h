@@ -191,6 +191,29 @@ __host__ __device__ inline int lse_tasks_per_seq(const Problem& P, int st) {
   return (P.HQ * nr + kLseRows - 1) / kLseRows;
 }
 
+// EXT passes: wave w of work-group blk takes task blk * 8 + w of the
+// (sequence, key tile, H_top head, extended row tile) tasks, in that order
+// (the row tiles of one head and key tile, which read the same keys, are
+// neighbours).  Returns the sequence; hm gets the task's head as a one-bit
+// mask, 0 past the last task.
+__device__ __forceinline__ int ext_task(const Problem& P, const StepArgs& a, const Seg& sg, int n_kt,
+                                        int blk, int& kt, int& rte, uint32_t& hm) {
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int per_kt = P.delta_eff * P.n_rt_x;
+  const int per_b = n_kt * per_kt;
+  const int ti = blk * 8 + w;
+  kt = 0;
+  rte = 0;
+  hm = 0u;
+  if (ti >= P.batch * per_b) return 0;
+  const int b = ti / per_b, rem = ti % per_b;
+  kt = rem / per_kt;
+  const int q = rem % per_kt;
+  rte = q % P.n_rt_x;
+  hm = 1u << nth_bit(htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b), q / P.n_rt_x);
+  return b;
+}
+
 template <class TT, int D, int G>
 __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
   extern __shared__ __align__(16) char smem[];
@@ -234,16 +257,21 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
       break;
     }
     case ST_PASS1:
-    case ST_P1B:
-    case ST_P1X: {
-      const Part part = st == ST_P1B ? PART_BASE : st == ST_P1X ? PART_EXT : PART_ALL;
-      const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
+    case ST_P1B: {
+      const Part part = st == ST_P1B ? PART_BASE : PART_ALL;
+      const int n_rtg = part == PART_BASE ? P.n_rtg_base : P.n_rtg;
       const int per_b = P.n_kt1 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
-      const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b) : 0u;
       score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot, sg.step), b, rem / n_rtg, rem % n_rtg,
-                              reinterpret_cast<float*>(smem), part, hm);
+                              reinterpret_cast<float*>(smem), part, 0u);
+      break;
+    }
+    case ST_P1X: {
+      int kt, rte;
+      uint32_t hm;
+      const int b = ext_task(P, a, sg, P.n_kt1, blk, kt, rte, hm);
+      score_tile<TT, D, G, 1>(P, score_io(a, sg.layer, sg.slot, sg.step), b, kt, rte,
+                              reinterpret_cast<float*>(smem), PART_EXT, hm);
       break;
     }
     case ST_LSE:
@@ -263,19 +291,24 @@ __global__ __launch_bounds__(kThreads) void step_kernel(StepArgs a) {
                            htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b));
       break;
     }
-    case ST_PASS2:
-    case ST_P2B:
     case ST_P2X: {
-      const Part part = st == ST_P2B ? PART_BASE : st == ST_P2X ? PART_EXT : PART_ALL;
-      const int n_rtg = part == PART_BASE ? P.n_rtg_base : part == PART_EXT ? P.n_rtg_x : P.n_rtg;
+      int kt, rte;
+      uint32_t hm;
+      const int b = ext_task(P, a, sg, P.n_kt2, blk, kt, rte, hm);
+      score_tile<TT, D, G, 2>(P, score_io(a, sg.layer, sg.slot, sg.step), b, kt, rte,
+                              reinterpret_cast<float*>(smem), PART_EXT, hm);
+      break;
+    }
+    case ST_PASS2:
+    case ST_P2B: {
+      const Part part = st == ST_P2B ? PART_BASE : PART_ALL;
+      const int n_rtg = part == PART_BASE ? P.n_rtg_base : P.n_rtg;
       const int per_b = P.n_kt2 * n_rtg;
       const int b = blk / per_b, rem = blk % per_b;
       const ScoreIO io = score_io(a, sg.layer, sg.slot, sg.step);
-      const uint32_t hm =
-          part == PART_EXT ? htop_mask(P, select_io(a, sg.layer, sg.slot, sg.step).stats, b) : 0u;
       score_tile<TT, D, G, 2>(P, io, b, rem / n_rtg, rem % n_rtg, reinterpret_cast<float*>(smem),
-                              part, hm);
-      if (part != PART_EXT) {
+                              part, 0u);
+      {
         // Clear this sequence's histograms for the pool stages of this layer.
         uint32_t* hist = reinterpret_cast<uint32_t*>(a.ws + (size_t)sg.slot * a.w.slot_bytes + a.w.hist) +
                          (int64_t)b * 2 * P.H * kHistBins;
